@@ -1,0 +1,197 @@
+"""Benchmark: relation-set following forward + backward on one MI355X.
+
+One step = kb_follow (forward, Eq. 4) + kb_follow_backward (dX and dR) over
+the whole KB for one minibatch, inputs already resident in HBM.  The default
+workload is the large KB: 10 M entities, 600 relations, 50 M distinct triples
+with Zipf subject/object/relation marginals, b = 32, 1 %-dense X.
+
+Prints one JSON line with the whole-step throughput (triple-batch products per
+second, N_T * b / step time), a roofline entry for the dominant kernel (HIP
+event time inside the timed region) and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "triple·batch products/sec for kb_follow fwd+bwd; achieved HBM GB/s vs peak"
+PEAK_HBM_GBPS = 8000.0
+DOMINANT_KERNEL_NAMES = {
+    "fwd_pieces": "pieces_kernel (forward: objects, gathers X)",
+    "dx_pieces": "pieces_kernel (dX: subjects, gathers dY)",
+    "dr_pieces": "pieces_kernel (dR: relations, gathers X and dY)",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pass_bytes(kb, b, phase):
+    """Algorithmic bytes of one pieces-kernel launch (gather model: every
+    triple's b-wide operand rows come from memory; plus the index stream and
+    the output rows), and the compulsory model (each distinct row once)."""
+    n_t, n_e, n_r = kb.n_triples, kb.n_entities, kb.n_relations
+    idx = 8 * n_t
+    if phase in ("fwd_pieces", "dx_pieces"):
+        gather = idx + 4 * (n_e + 1) + 4 * b * n_t + 4 * b * n_e      # A gathered per triple, R from LDS/L2
+        a_ids = kb.subj if phase == "fwd_pieces" else kb.obj
+        out_ids = kb.obj if phase == "fwd_pieces" else kb.subj
+        comp = idx + 4 * (n_e + 1) + 4 * b * len(np.unique(a_ids)) + 4 * b * n_r \
+            + 4 * b * len(np.unique(out_ids))
+    else:
+        gather = idx + 4 * (n_r + 1) + 8 * b * n_t + 4 * b * n_r
+        comp = idx + 4 * (n_r + 1) + 4 * b * (len(np.unique(kb.subj)) + len(np.unique(kb.obj))) \
+            + 4 * b * n_r
+    return float(gather), float(comp)
+
+
+def cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads):
+    import oracle
+    s, r, o = kb.subj, kb.rel, kb.obj
+    n_e, n_r = kb.n_entities, kb.n_relations
+    Xs, Rs, dYs = X_bm[:cols], R_bm[:cols], dY_bm[:cols]
+    oracle.follow(s[:1000], r[:1000], o[:1000], n_e, n_r, Xs[:1], Rs[:1])  # load + warm
+    t0 = time.perf_counter()
+    oracle.follow(s, r, o, n_e, n_r, Xs, Rs, nthreads=threads)
+    oracle.follow_backward(s, r, o, n_e, n_r, Xs, Rs, dYs, nthreads=threads)
+    dt = time.perf_counter() - t0
+    return {
+        "value": kb.n_triples * cols / dt,
+        "unit": "triple·batch/s",
+        "cores": int(min(threads, cols)),
+        "kind": "oracle",
+        "sample": (f"same KB, {cols} of {X_bm.shape[0]} batch columns, forward + dX + dR, "
+                   f"{dt:.1f} s on {min(threads, cols)} threads of {os.cpu_count()} "
+                   f"({platform.processor() or platform.machine()})"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="large",
+                    help="tiny | metaqa | large | train (kbgen workload names)")
+    ap.add_argument("--cpu-cols", type=int, default=8, help="batch columns the oracle times")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip the HIP-event phase timing")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the follow path here has no multi-GPU sharding "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import kbgen
+    import paper_2002_06115_amd as kbf
+
+    w = kbgen.WORKLOADS[args.workload]
+    if w.name == "chain3":
+        raise SystemExit("chain3 is a parity case, not a bench workload")
+    t0 = time.perf_counter()
+    kb = kbgen.make_kb(w)
+    X_bm, R_bm, dY_bm = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
+    log(f"[bench] generated {w.label} in {time.perf_counter() - t0:.1f} s; stats {kb.stats()}")
+
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
+    torch.cuda.synchronize()
+    create_s = time.perf_counter() - t0
+    log(f"[bench] kb_create {create_s:.1f} s, info {gkb.info()}")
+    em = lambda a: torch.from_numpy(a).cuda().t().contiguous()
+    X, R, dY = em(X_bm), em(R_bm), em(dY_bm)
+    b = w.batch
+    Y = torch.empty_like(X)
+    dX = torch.empty_like(X)
+    dR = torch.empty_like(R)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gkb.follow(X, R, out=Y, stream=stream)
+        gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} done")
+
+    if not args.no_profile:
+        gkb.profile(True)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    phases = gkb.profile_read() if not args.no_profile else {}
+    gkb.profile(False)
+    ms_step = ms_total / args.steps
+    value = kb.n_triples * b / (ms_step * 1e-3)
+    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.3e} triple*batch/s")
+
+    roof = None
+    if phases:
+        dom = max(("fwd_pieces", "dx_pieces", "dr_pieces"), key=lambda p: phases[p][0])
+        ms_avg = phases[dom][0] / max(1, phases[dom][1])
+        gather_b, comp_b = pass_bytes(kb, b, dom)
+        achieved = gather_b / (ms_avg * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                "kernel": DOMINANT_KERNEL_NAMES[dom], "kernel_ms": round(ms_avg, 4),
+                "bytes_model": "gather: 8 B of ids per triple + every triple's gathered "
+                               "b-wide rows + output rows",
+                "algorithmic_bytes": gather_b,
+                "compulsory_bytes": comp_b,
+                "compulsory_GBps": round(comp_b / (ms_avg * 1e-3) / 1e9, 1)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cols = max(1, min(args.cpu_cols, b))
+        threads = min(cols, os.cpu_count() or 1)
+        log(f"[bench] timing the CPU oracle on {cols} batch columns, {threads} threads")
+        cpu = cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads)
+        log(f"[bench] oracle {cpu['value']:.3e} triple*batch/s")
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "triple·batch/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 in/out, f64 accumulate",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n_entities": w.n_entities, "n_relations": w.n_relations,
+                   "n_triples": kb.n_triples, "batch": b,
+                   "laws": {"subj": w.subj_law, "obj": w.obj_law, "rel": w.rel_law},
+                   "x": w.x_kind, "r": w.r_kind, "dy": w.dy_kind, "parallelism": "single GPU"},
+        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+        "kb_create_s": round(create_s, 2),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

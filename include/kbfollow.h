@@ -1,0 +1,198 @@
+/*
+ * kbfollow.h -- C ABI of the MI355X (gfx950) relation-set following library.
+ *
+ * A reified KB (Sec. 2.3) stores N_T triples (s_l, r_l, o_l): subject entity,
+ * relation and object entity of fact l.  With M_subj, M_obj, M_rel the N_T x N_E,
+ * N_T x N_E and N_T x N_R matrices that map triple l to its subject, object and
+ * relation (M_rel holding the triple's weight w_l for a soft KB, App. A), the
+ * library evaluates for a minibatch of b examples (Eq. 4, App. C)
+ *
+ *     Y = follow(X, R) = (X M_subj^T  (.)  R M_rel^T) M_obj
+ *
+ * and the two gradients of a scalar loss with upstream gradient dY = dL/dY:
+ *
+ *     dX[i] = sum over triples l with s_l == i of  w_l * dY[o_l] (.) R[r_l]
+ *     dR[k] = sum over triples l with r_l == k of  w_l * X[s_l]  (.) dY[o_l]
+ *
+ * Layout of every activation (this library's own choice, the transpose of the
+ * paper's b x N row-vector view): entity-major, batch-contiguous float32.
+ *     X, Y, dY, dX : [N_E][b]   element (i, beta) at i * b + beta
+ *     R, dR        : [N_R][b]   element (k, beta) at k * b + beta
+ * Ids are 0-based (the paper's are 1-based, Sec. 2.1).
+ *
+ * Numerics: products and sums are taken in double precision on the GPU and
+ * every output element is rounded to float once.  Sums run in a fixed order,
+ * so two calls with the same inputs give bitwise-equal results.  Duplicate
+ * triples each count.  An output row no triple reaches is +0.0.  No clamping
+ * and no NaN checks: IEEE values propagate.
+ *
+ * Streams: every compute call only enqueues work on `stream` (a hipStream_t;
+ * NULL = the null stream) and returns; it never synchronises the host and
+ * never allocates device memory.  Scratch space comes from the caller's
+ * `workspace`, sized with kb_workspace_size().
+ *
+ * Errors: argument checks run on the host before anything is enqueued; on
+ * failure nothing is launched and no output is touched.  The status says what
+ * went wrong and kb_last_error() gives a message (per calling thread).
+ * No C++ exception ever crosses this interface.
+ *
+ * Thread safety: a kb_t is immutable after kb_create (profiling counters
+ * excepted, see kb_profile_*), so calls on different streams, each with its
+ * own workspace and outputs, may run concurrently.
+ */
+#ifndef KBFOLLOW_H
+#define KBFOLLOW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct kb_t kb_t; /* opaque handle to a KB resident on one GPU */
+
+typedef enum {
+  KB_OK = 0,
+  KB_EINVAL = 1,  /* bad argument: null pointer, size, alignment, overlap, workspace */
+  KB_ERANGE = 2,  /* a triple id outside [0, N_E) or [0, N_R) */
+  KB_ENOMEM = 3,  /* device or host allocation failed */
+  KB_EHIP = 4,    /* a HIP runtime call or kernel launch failed */
+  KB_ENOTSUP = 5  /* valid request this build does not implement */
+} kb_status;
+
+/*
+ * Build a KB on the current HIP device from host triple arrays (Sec. 2.3: the
+ * reified KB M_subj, M_obj, M_rel, one nonzero per row).
+ *
+ *   n_entities, n_relations : N_E >= 0 and N_R >= 0, each below 2^31.
+ *   n_triples               : N_T, 0 <= N_T < 2^31.
+ *   subj, rel, obj          : HOST int32 arrays of N_T ids (may be NULL when
+ *                             N_T == 0); copied, the caller keeps ownership.
+ *   weight                  : HOST float array of N_T triple weights w_l
+ *                             (soft KB, App. A) or NULL for a hard KB (w = 1).
+ *   stream                  : hipStream_t used for the uploads.  kb_create
+ *                             waits for them before it returns.
+ *   out                     : receives the handle; set to NULL on failure.
+ *
+ * The three sorted layouts (by object, by subject, by relation) and their
+ * work plans are built on the host and uploaded; the host copies are freed.
+ * Errors: KB_EINVAL (sizes, null pointers), KB_ERANGE (an id out of range;
+ * checked before any device work), KB_ENOMEM, KB_EHIP.
+ */
+kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
+                    const int32_t *subj, const int32_t *rel, const int32_t *obj,
+                    const float *weight, void *stream, kb_t **out);
+
+/* Free a KB and its device memory.  NULL-safe.  The caller must make sure no
+ * enqueued work still uses it (synchronise its streams first). */
+void kb_destroy(kb_t *kb);
+
+/* Bytes of device workspace that kb_follow and kb_follow_backward need for
+ * batch size b (scratch for the partial sums of rows split into pieces).  May
+ * be 0.  Returns 0 for a NULL kb or b < 1. */
+size_t kb_workspace_size(const kb_t *kb, int32_t b);
+
+/*
+ * Forward pass, Eq. 4:  Y[j] = sum over triples l with o_l == j of
+ * w_l * X[s_l] (.) R[r_l]   (b-wide rows).
+ *
+ *   b          : batch size, b >= 1.
+ *   X          : DEVICE float [N_E][b], read only.
+ *   R          : DEVICE float [N_R][b], read only.
+ *   Y          : DEVICE float [N_E][b], fully overwritten; must not overlap X or R.
+ *   workspace  : DEVICE scratch of at least kb_workspace_size(kb, b) bytes,
+ *                256-byte aligned (may be NULL when that size is 0).  Its
+ *                contents on entry are ignored.  Calls running at the same
+ *                time must not share one.
+ *   ws_bytes   : size of workspace in bytes.
+ *   stream     : hipStream_t on which the work is enqueued.
+ *
+ * Pointers must be 4-byte aligned; when b % 4 == 0 the fast path also needs
+ * X, R and Y 16-byte aligned (otherwise KB_EINVAL).
+ */
+kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, float *Y,
+                    void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Backward pass of Eq. 4 for upstream gradient dY:
+ *   dX[i] = sum over l with s_l == i of w_l * dY[o_l] (.) R[r_l]
+ *   dR[k] = sum over l with r_l == k of w_l * X[s_l] (.) dY[o_l]
+ *
+ *   X, R, dY : DEVICE float [N_E][b], [N_R][b], [N_E][b], read only.  X may be
+ *              NULL when dR is NULL, R may be NULL when dX is NULL.
+ *   dX       : DEVICE float [N_E][b], overwritten, or NULL to skip it.
+ *   dR       : DEVICE float [N_R][b], overwritten, or NULL to skip it.
+ *   Outputs must not overlap each other or any input.  Workspace and stream as
+ *   for kb_follow (dX and dR reuse the same workspace one after the other).
+ */
+kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const float *R,
+                             const float *dY, float *dX, float *dR, void *workspace,
+                             size_t ws_bytes, void *stream);
+
+/* Static description of a status code. */
+const char *kb_status_str(kb_status s);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char *kb_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Inspection (host side; none of these touch the GPU)
+ * ------------------------------------------------------------------------ */
+
+/* Sizes and plan statistics of a built KB. */
+typedef struct {
+  int64_t n_entities, n_relations, n_triples;
+  int32_t weighted;         /* 1 if built with per-triple weights */
+  int32_t piece_len[3];     /* longest piece of a row one lane group sums (obj, subj, rel) */
+  int64_t n_pieces[3];      /* work items per layout: by object, by subject, by relation */
+  int64_t n_split_rows[3];  /* rows cut into more than one piece */
+  int64_t n_slots[3];       /* partial-sum slots (all combine levels) */
+  int32_t n_levels[3];      /* combine levels */
+  int64_t n_empty_rows[3];  /* rows with no triple (written as zeros) */
+  int64_t max_row_len[3];   /* longest row (triples) */
+  int64_t device_bytes;     /* device memory the KB holds */
+} kb_info_t;
+
+kb_status kb_get_info(const kb_t *kb, kb_info_t *info);
+
+/*
+ * The sorted layout kb_create builds, computed on the host only (no GPU needed).
+ *   which = 0: by object  (rows = objects,   key order (o, s, r)), col_a = subj, col_b = rel
+ *   which = 1: by subject (rows = subjects,  key order (s, o, r)), col_a = obj,  col_b = rel
+ *   which = 2: by relation(rows = relations, key order (r, s, o)), col_a = subj, col_b = obj
+ *   offsets : HOST int32 [rows + 1]; row q's triples are positions offsets[q] .. offsets[q+1]-1
+ *   col_a, col_b, perm : HOST int32 [N_T]; perm[p] = caller index of the triple at position p
+ * Any output pointer may be NULL.  Same validation and errors as kb_create.
+ */
+kb_status kb_layout_host(int64_t n_entities, int64_t n_relations, int64_t n_triples,
+                         const int32_t *subj, const int32_t *rel, const int32_t *obj,
+                         int32_t which, int32_t *offsets, int32_t *col_a, int32_t *col_b,
+                         int32_t *perm);
+
+/* ------------------------------------------------------------------------
+ * Kernel timing with HIP events (for benchmarks; not thread safe)
+ * ------------------------------------------------------------------------ */
+
+/* Phases whose GPU time is recorded when profiling is on. */
+typedef enum {
+  KB_PH_FWD_PIECES = 0, KB_PH_FWD_COMBINE, KB_PH_FWD_ZERO,
+  KB_PH_DX_PIECES, KB_PH_DX_COMBINE, KB_PH_DX_ZERO,
+  KB_PH_DR_PIECES, KB_PH_DR_COMBINE, KB_PH_DR_ZERO,
+  KB_PH_COUNT
+} kb_phase;
+
+/* Turn event recording around each phase's launches on (1) or off (0).
+ * Turning it on clears the accumulated times. */
+kb_status kb_profile_enable(kb_t *kb, int32_t on);
+
+/* Wait for the recorded events, add their elapsed times into ms[KB_PH_COUNT]
+ * and their launch counts into launches[KB_PH_COUNT] (either may be NULL),
+ * then clear the record. */
+kb_status kb_profile_read(kb_t *kb, double *ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KBFOLLOW_H */

@@ -1,0 +1,276 @@
+"""Relation-set following on a reified knowledge base, for MI355X (gfx950).
+
+A thin ctypes binding over ``libkbfollow.so`` (declared in
+``include/kbfollow.h``): argument marshalling only, every step of the
+computation runs in the library's HIP kernels.  PyTorch supplies device memory
+and the current stream.
+
+    kb = KB(subj, rel, obj, n_entities, n_relations)        # host int32 triples
+    Y  = kb.follow(X, R)                                    # X [N_E][b], R [N_R][b]
+    dX, dR = kb.follow_backward(X, R, dY)
+    Y  = follow(kb, X, R)                                   # autograd-aware
+
+Activations are entity-major and batch-contiguous float32 CUDA tensors:
+``X[i, beta]`` is the weight of entity i in example beta (the transpose of the
+paper's ``b x N_E`` minibatch, App. C).  The library never falls back to any
+other implementation: if it is not built, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "_lib", "libkbfollow.so")
+
+KB_OK, KB_EINVAL, KB_ERANGE, KB_ENOMEM, KB_EHIP, KB_ENOTSUP = range(6)
+PHASES = ("fwd_pieces", "fwd_combine", "fwd_zero", "dx_pieces", "dx_combine", "dx_zero",
+          "dr_pieces", "dr_combine", "dr_zero")
+
+
+class KBError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class KBInfo(ctypes.Structure):
+    _fields_ = [("n_entities", ctypes.c_int64), ("n_relations", ctypes.c_int64),
+                ("n_triples", ctypes.c_int64), ("weighted", ctypes.c_int32),
+                ("piece_len", ctypes.c_int32 * 3), ("n_pieces", ctypes.c_int64 * 3),
+                ("n_split_rows", ctypes.c_int64 * 3), ("n_slots", ctypes.c_int64 * 3),
+                ("n_levels", ctypes.c_int32 * 3), ("n_empty_rows", ctypes.c_int64 * 3),
+                ("max_row_len", ctypes.c_int64 * 3), ("device_bytes", ctypes.c_int64)]
+
+    def as_dict(self):
+        d = {}
+        for name, _ in self._fields_:
+            v = getattr(self, name)
+            d[name] = list(v) if hasattr(v, "__len__") else int(v)
+        return d
+
+
+def _load_library():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2002_06115_amd.build` "
+                          "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, i32, p, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+    lib.kb_create.argtypes = [i64, i64, i64, p, p, p, p, p, ctypes.POINTER(p)]
+    lib.kb_create.restype = ctypes.c_int
+    lib.kb_destroy.argtypes = [p]
+    lib.kb_destroy.restype = None
+    lib.kb_workspace_size.argtypes = [p, i32]
+    lib.kb_workspace_size.restype = sz
+    lib.kb_follow.argtypes = [p, i32, p, p, p, p, sz, p]
+    lib.kb_follow.restype = ctypes.c_int
+    lib.kb_follow_backward.argtypes = [p, i32, p, p, p, p, p, p, sz, p]
+    lib.kb_follow_backward.restype = ctypes.c_int
+    lib.kb_status_str.argtypes = [ctypes.c_int]
+    lib.kb_status_str.restype = ctypes.c_char_p
+    lib.kb_last_error.argtypes = []
+    lib.kb_last_error.restype = ctypes.c_char_p
+    lib.kb_get_info.argtypes = [p, ctypes.POINTER(KBInfo)]
+    lib.kb_get_info.restype = ctypes.c_int
+    lib.kb_layout_host.argtypes = [i64, i64, i64, p, p, p, i32, p, p, p, p]
+    lib.kb_layout_host.restype = ctypes.c_int
+    lib.kb_profile_enable.argtypes = [p, i32]
+    lib.kb_profile_enable.restype = ctypes.c_int
+    lib.kb_profile_read.argtypes = [p, p, p]
+    lib.kb_profile_read.restype = ctypes.c_int
+    return lib
+
+
+_lib = _load_library()
+
+
+def _check(status, what):
+    if status != KB_OK:
+        detail = _lib.kb_last_error().decode()
+        raise KBError(status, f"{what}: {_lib.kb_status_str(status).decode()}: {detail}")
+
+
+def _host_ids(a, n):
+    a = np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+    if a.shape != (n,):
+        raise ValueError("subj, rel and obj must be 1-D arrays of equal length")
+    return a
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def layout_host(subj, rel, obj, n_entities, n_relations, which):
+    """The sorted layout the library builds (host only): (offsets, col_a, col_b, perm)."""
+    n_t = len(subj)
+    subj, rel, obj = (_host_ids(a, n_t) for a in (subj, rel, obj))
+    rows = n_relations if which == 2 else n_entities
+    off = np.empty(rows + 1, np.int32)
+    ca, cb, perm = (np.empty(n_t, np.int32) for _ in range(3))
+    _check(_lib.kb_layout_host(n_entities, n_relations, n_t, _np_ptr(subj), _np_ptr(rel),
+                               _np_ptr(obj), which, _np_ptr(off), _np_ptr(ca), _np_ptr(cb),
+                               _np_ptr(perm)), "kb_layout_host")
+    return off, ca, cb, perm
+
+
+class KB:
+    """A reified KB resident on one GPU (Sec. 2.3): N_T triples (subj, rel, obj)."""
+
+    def __init__(self, subj, rel, obj, n_entities, n_relations, weight=None, device=None):
+        import torch
+        n_t = len(subj)
+        subj, rel, obj = (_host_ids(a, n_t) for a in (subj, rel, obj))
+        w = None if weight is None else np.ascontiguousarray(weight, dtype=np.float32)
+        if w is not None and w.shape != (n_t,):
+            raise ValueError("weight must have one entry per triple")
+        self.device = torch.device("cuda", torch.cuda.current_device()) if device is None \
+            else torch.device(device)
+        self.n_entities, self.n_relations, self.n_triples = int(n_entities), int(n_relations), n_t
+        self._ws = {}
+        self._handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            stream = torch.cuda.current_stream(self.device).cuda_stream
+            _check(_lib.kb_create(self.n_entities, self.n_relations, n_t, _np_ptr(subj),
+                                  _np_ptr(rel), _np_ptr(obj), _np_ptr(w), ctypes.c_void_p(stream),
+                                  ctypes.byref(self._handle)), "kb_create")
+
+    def close(self):
+        if getattr(self, "_handle", None) and self._handle.value:
+            import torch
+            torch.cuda.synchronize(self.device)
+            _lib.kb_destroy(self._handle)
+            self._handle = ctypes.c_void_p()
+            self._ws.clear()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- helpers -------------------------------------------------------------
+    def info(self):
+        inf = KBInfo()
+        _check(_lib.kb_get_info(self._handle, ctypes.byref(inf)), "kb_get_info")
+        return inf.as_dict()
+
+    def workspace_size(self, b):
+        return int(_lib.kb_workspace_size(self._handle, int(b)))
+
+    def workspace(self, b):
+        """A cached device workspace for batch size b (uint8 tensor or None)."""
+        import torch
+        n = self.workspace_size(b)
+        if n == 0:
+            return None
+        ws = self._ws.get(b)
+        if ws is None or ws.numel() < n:
+            ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+            self._ws[b] = ws
+        return ws
+
+    def _act(self, t, rows, name):
+        import torch
+        if t is None:
+            return None
+        if not isinstance(t, torch.Tensor) or t.dtype != torch.float32 or t.device != self.device:
+            raise TypeError(f"{name} must be a float32 tensor on {self.device}")
+        if t.dim() != 2 or t.shape[0] != rows or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous [{rows}][b] tensor")
+        return t
+
+    @staticmethod
+    def _ptr(t):
+        return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+    # -- the operations --------------------------------------------------------
+    def follow(self, X, R, out=None, stream=None):
+        """Y = follow(X, R) (Eq. 4) for X [N_E][b], R [N_R][b]; returns Y [N_E][b]."""
+        import torch
+        X = self._act(X, self.n_entities, "X")
+        R = self._act(R, self.n_relations, "R")
+        b = X.shape[1]
+        if R.shape[1] != b:
+            raise ValueError("X and R must have the same batch size")
+        Y = torch.empty_like(X) if out is None else self._act(out, self.n_entities, "out")
+        ws = self.workspace(b)
+        s = torch.cuda.current_stream(self.device) if stream is None else stream
+        with torch.cuda.device(self.device):
+            _check(_lib.kb_follow(self._handle, b, self._ptr(X), self._ptr(R), self._ptr(Y),
+                                  self._ptr(ws), 0 if ws is None else ws.numel(),
+                                  ctypes.c_void_p(s.cuda_stream)), "kb_follow")
+        return Y
+
+    def follow_backward(self, X, R, dY, want_dx=True, want_dr=True, dX=None, dR=None,
+                        stream=None):
+        """(dX [N_E][b], dR [N_R][b]) for upstream gradient dY [N_E][b]."""
+        import torch
+        dY = self._act(dY, self.n_entities, "dY")
+        b = dY.shape[1]
+        X = self._act(X, self.n_entities, "X") if want_dr else None
+        R = self._act(R, self.n_relations, "R") if want_dx else None
+        if want_dx and dX is None:
+            dX = torch.empty((self.n_entities, b), dtype=torch.float32, device=self.device)
+        if want_dr and dR is None:
+            dR = torch.empty((self.n_relations, b), dtype=torch.float32, device=self.device)
+        dX = self._act(dX, self.n_entities, "dX") if want_dx else None
+        dR = self._act(dR, self.n_relations, "dR") if want_dr else None
+        ws = self.workspace(b)
+        s = torch.cuda.current_stream(self.device) if stream is None else stream
+        with torch.cuda.device(self.device):
+            _check(_lib.kb_follow_backward(self._handle, b, self._ptr(X), self._ptr(R),
+                                           self._ptr(dY), self._ptr(dX), self._ptr(dR),
+                                           self._ptr(ws), 0 if ws is None else ws.numel(),
+                                           ctypes.c_void_p(s.cuda_stream)),
+                   "kb_follow_backward")
+        return dX, dR
+
+    # -- event timing -----------------------------------------------------------
+    def profile(self, on=True):
+        _check(_lib.kb_profile_enable(self._handle, 1 if on else 0), "kb_profile_enable")
+
+    def profile_read(self):
+        """{phase: (total ms, launches)} since the last read."""
+        ms = (ctypes.c_double * len(PHASES))()
+        n = (ctypes.c_int64 * len(PHASES))()
+        _check(_lib.kb_profile_read(self._handle, ctypes.cast(ms, ctypes.c_void_p),
+                                    ctypes.cast(n, ctypes.c_void_p)), "kb_profile_read")
+        return {p: (ms[i], n[i]) for i, p in enumerate(PHASES)}
+
+
+def _make_function():
+    import torch
+
+    class _Follow(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, X, R, kb):
+            ctx.kb = kb
+            ctx.save_for_backward(X, R)
+            return kb.follow(X, R)
+
+        @staticmethod
+        def backward(ctx, dY):
+            X, R = ctx.saved_tensors
+            need_x, need_r = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
+            dX, dR = ctx.kb.follow_backward(X, R, dY.contiguous(), want_dx=need_x,
+                                            want_dr=need_r)
+            return dX, dR, None
+
+    return _Follow
+
+
+_FollowFn = None
+
+
+def follow(kb: KB, X, R):
+    """Differentiable follow(X, R) (Eq. 4) on entity-major tensors X [N_E][b], R [N_R][b]."""
+    global _FollowFn
+    if _FollowFn is None:
+        _FollowFn = _make_function()
+    return _FollowFn.apply(X, R, kb)
+
+
+__all__ = ["KB", "KBError", "follow", "layout_host", "LIB_PATH", "PHASES"]

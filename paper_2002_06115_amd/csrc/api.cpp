@@ -1,0 +1,483 @@
+// api.cpp -- the C ABI of kbfollow.h: KB construction, the three passes,
+// workspace sizing, errors and event-based kernel timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kbfollow.h"
+#include "kernels.h"
+#include "plan.h"
+
+using namespace kbf;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kb_status fail(kb_status s, const std::string &msg) {
+  g_last_error = msg;
+  return s;
+}
+
+kb_status hip_fail(hipError_t e, const char *what) {
+  return fail(KB_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Work plan of one layout, resident on the device.
+struct DevLayout {
+  int64_t rows = 0;
+  int2 *pairs = nullptr;      // (gathered id, second id) per position
+  float *weight = nullptr;    // per position or nullptr
+  int4 *pieces = nullptr;
+  int64_t n_pieces = 0;
+  int32_t *empty = nullptr;
+  int64_t n_empty = 0;
+  int4 *ctasks = nullptr;     // all combine levels, back to back
+  std::vector<int64_t> level_begin;  // host: level L is [level_begin[L], level_begin[L+1])
+  int64_t n_slots = 0;
+  int64_t n_split_rows = 0;
+  int64_t max_row_len = 0;
+  int32_t piece_len = 0;
+};
+
+struct Timing {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  struct Rec {
+    int phase;
+    hipEvent_t start, stop;
+  };
+  std::vector<Rec> recs;
+};
+
+int env_int(const char *name, int dflt) {
+  const char *v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  return std::atoi(v);
+}
+
+}  // namespace
+
+struct kb_t {
+  int device = 0;
+  int n_cu = 0;
+  size_t lds_per_block = 0;
+  size_t lds_per_cu = 0;
+  int64_t n_entities = 0, n_relations = 0, n_triples = 0;
+  bool weighted = false;
+  int b_in_lds_mode = -1;  // -1 auto, 0 never, 1 whenever it fits
+  DevLayout L[3];
+  std::vector<void *> allocations;
+  int64_t device_bytes = 0;
+  mutable Timing timing;
+};
+
+namespace {
+
+template <class T>
+kb_status upload(kb_t *kb, const std::vector<T> &host, T **dev, hipStream_t s) {
+  *dev = nullptr;
+  if (host.empty()) return KB_OK;
+  const size_t bytes = host.size() * sizeof(T);
+  void *p = nullptr;
+  hipError_t e = hipMalloc(&p, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(KB_ENOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+  }
+  kb->allocations.push_back(p);
+  kb->device_bytes += (int64_t)bytes;
+  e = hipMemcpyAsync(p, host.data(), bytes, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  *dev = static_cast<T *>(p);
+  return KB_OK;
+}
+
+void free_kb(kb_t *kb) {
+  for (void *p : kb->allocations) (void)hipFree(p);
+  for (hipEvent_t ev : kb->timing.pool) (void)hipEventDestroy(ev);
+  for (auto &r : kb->timing.recs) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  delete kb;
+}
+
+kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32_t piece_len,
+                              int32_t fan_in, hipStream_t s) {
+  PlanHost P = plan_layout(H, piece_len, fan_in);
+  D.rows = H.rows;
+  D.piece_len = piece_len;
+  D.n_pieces = (int64_t)P.pieces.size();
+  D.n_empty = (int64_t)P.empty_rows.size();
+  D.n_slots = P.n_slots;
+  D.n_split_rows = P.n_split_rows;
+  D.max_row_len = P.max_row_len;
+  std::vector<int2> pairs(H.col_a.size());
+  for (size_t p = 0; p < pairs.size(); ++p) pairs[p] = make_int2(H.col_a[p], H.col_b[p]);
+  std::vector<int4> pieces(P.pieces.size());
+  for (size_t i = 0; i < pieces.size(); ++i)
+    pieces[i] = make_int4(P.pieces[i].start, P.pieces[i].len, P.pieces[i].dst, 0);
+  std::vector<int4> ctasks;
+  D.level_begin.assign(1, 0);
+  for (const auto &lv : P.levels) {
+    for (const CombineTask &c : lv) ctasks.push_back(make_int4(c.first, c.n, c.dst, 0));
+    D.level_begin.push_back((int64_t)ctasks.size());
+  }
+  kb_status st;
+  if ((st = upload(kb, pairs, &D.pairs, s)) != KB_OK) return st;
+  if ((st = upload(kb, H.weight, &D.weight, s)) != KB_OK) return st;
+  if ((st = upload(kb, pieces, &D.pieces, s)) != KB_OK) return st;
+  if ((st = upload(kb, P.empty_rows, &D.empty, s)) != KB_OK) return st;
+  if ((st = upload(kb, ctasks, &D.ctasks, s)) != KB_OK) return st;
+  // The host vectors die with this frame: wait for the copies first.
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  return KB_OK;
+}
+
+// Event bracket around one phase's launches.
+struct PhaseScope {
+  const kb_t *kb;
+  int phase;
+  hipStream_t s;
+  hipEvent_t start = nullptr, stop = nullptr;
+  static hipEvent_t take(Timing &t) {
+    if (!t.pool.empty()) {
+      hipEvent_t e = t.pool.back();
+      t.pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  PhaseScope(const kb_t *k, int ph, hipStream_t st) : kb(k), phase(ph), s(st) {
+    if (!kb->timing.on) return;
+    start = take(kb->timing);
+    stop = take(kb->timing);
+    if (start) (void)hipEventRecord(start, s);
+  }
+  ~PhaseScope() {
+    if (!start || !stop) return;
+    (void)hipEventRecord(stop, s);
+    kb->timing.recs.push_back({phase, start, stop});
+  }
+};
+
+bool overlaps(const void *a, size_t abytes, const void *b, size_t bbytes) {
+  if (!a || !b || !abytes || !bbytes) return false;
+  const char *pa = static_cast<const char *>(a), *pb = static_cast<const char *>(b);
+  return pa < pb + bbytes && pb < pa + abytes;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+kb_status check_device(const kb_t *kb) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != kb->device)
+    return fail(KB_EINVAL, "the current HIP device is " + std::to_string(dev) +
+                               " but the KB lives on device " + std::to_string(kb->device));
+  return KB_OK;
+}
+
+// Runs one pass: pieces, combine levels, empty rows.
+kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float *A,
+                   const float *B, int64_t B_rows, bool b_may_use_lds, int32_t b, float *out,
+                   void *ws, hipStream_t s) {
+  double *slots = static_cast<double *>(ws);
+  {
+    PhaseScope scope(kb, ph_base + 0, s);
+    PiecesArgs a{D.pieces, D.n_pieces, D.pairs, D.weight, A, B, B_rows, b, out, slots};
+    bool lds = false;
+    int max_blocks = 0;
+    if (b_may_use_lds && kb->b_in_lds_mode != 0) {
+      const size_t bytes = pieces_lds_bytes(b, B_rows);
+      const size_t limit = kb->b_in_lds_mode == 1 ? kb->lds_per_block : std::min<size_t>(kb->lds_per_block, 64 * 1024);
+      if (bytes > 0 && bytes <= limit) {
+        lds = true;
+        const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(8, kb->lds_per_cu / bytes));
+        max_blocks = kb->n_cu * per_cu;
+        if (bytes > 64 * 1024) {
+          hipError_t e = prepare_pieces_lds(b, bytes);
+          if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
+        }
+      }
+    }
+    hipError_t e = launch_pieces(a, lds, max_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "pieces kernel launch");
+  }
+  {
+    PhaseScope scope(kb, ph_base + 1, s);
+    for (size_t L = 0; L + 1 < D.level_begin.size(); ++L) {
+      const int64_t n = D.level_begin[L + 1] - D.level_begin[L];
+      hipError_t e = launch_combine(D.ctasks + D.level_begin[L], n, slots, b, out, s);
+      if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
+    }
+  }
+  {
+    PhaseScope scope(kb, ph_base + 2, s);
+    hipError_t e = launch_zero_rows(D.empty, D.n_empty, b, out, s);
+    if (e != hipSuccess) return hip_fail(e, "zero-rows kernel launch");
+  }
+  return KB_OK;
+}
+
+size_t workspace_bytes(const kb_t *kb, int32_t b) {
+  int64_t slots = 0;
+  for (const DevLayout &D : kb->L) slots = std::max(slots, D.n_slots);
+  size_t bytes = (size_t)slots * (size_t)b * sizeof(double);
+  return (bytes + 255) / 256 * 256;
+}
+
+kb_status check_ws(const kb_t *kb, int32_t b, void *ws, size_t ws_bytes) {
+  const size_t need = workspace_bytes(kb, b);
+  if (need == 0) return KB_OK;
+  if (!ws) return fail(KB_EINVAL, "workspace is NULL but " + std::to_string(need) + " bytes are needed");
+  if (ws_bytes < need)
+    return fail(KB_EINVAL, "workspace has " + std::to_string(ws_bytes) + " bytes, " +
+                               std::to_string(need) + " are needed");
+  if (!aligned(ws, 16)) return fail(KB_EINVAL, "workspace must be 16-byte aligned");
+  return KB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *kb_status_str(kb_status s) {
+  switch (s) {
+    case KB_OK: return "ok";
+    case KB_EINVAL: return "invalid argument";
+    case KB_ERANGE: return "id out of range";
+    case KB_ENOMEM: return "out of memory";
+    case KB_EHIP: return "HIP runtime error";
+    case KB_ENOTSUP: return "not supported";
+  }
+  return "unknown status";
+}
+
+const char *kb_last_error(void) { return g_last_error.c_str(); }
+
+kb_status kb_layout_host(int64_t n_entities, int64_t n_relations, int64_t n_triples,
+                         const int32_t *subj, const int32_t *rel, const int32_t *obj,
+                         int32_t which, int32_t *offsets, int32_t *col_a, int32_t *col_b,
+                         int32_t *perm) {
+  try {
+    g_last_error.clear();
+    if (which < 0 || which > 2) return fail(KB_EINVAL, "which must be 0, 1 or 2");
+    bool range = false;
+    std::string msg = validate_triples(n_entities, n_relations, n_triples, subj, rel, obj, &range);
+    if (!msg.empty()) return fail(range ? KB_ERANGE : KB_EINVAL, msg);
+    LayoutHost L[3];
+    build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, nullptr, true, L);
+    const LayoutHost &H = L[which];
+    if (offsets) std::copy(H.offsets.begin(), H.offsets.end(), offsets);
+    if (col_a) std::copy(H.col_a.begin(), H.col_a.end(), col_a);
+    if (col_b) std::copy(H.col_b.begin(), H.col_b.end(), col_b);
+    if (perm) std::copy(H.perm.begin(), H.perm.end(), perm);
+    return KB_OK;
+  } catch (const std::bad_alloc &) {
+    return fail(KB_ENOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(KB_EINVAL, "unexpected host error");
+  }
+}
+
+kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
+                    const int32_t *subj, const int32_t *rel, const int32_t *obj,
+                    const float *weight, void *stream, kb_t **out) {
+  if (!out) return fail(KB_EINVAL, "out must be non-NULL");
+  *out = nullptr;
+  kb_t *kb = nullptr;
+  try {
+    g_last_error.clear();
+    bool range = false;
+    std::string msg = validate_triples(n_entities, n_relations, n_triples, subj, rel, obj, &range);
+    if (!msg.empty()) return fail(range ? KB_ERANGE : KB_EINVAL, msg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    kb = new kb_t();
+    hipError_t e = hipGetDevice(&kb->device);
+    if (e != hipSuccess) {
+      free_kb(kb);
+      return hip_fail(e, "hipGetDevice");
+    }
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, kb->device) == hipSuccess)
+      kb->n_cu = v;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, kb->device) == hipSuccess)
+      kb->lds_per_block = (size_t)v;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, kb->device) == hipSuccess)
+      kb->lds_per_cu = (size_t)v;
+    if (kb->lds_per_cu < kb->lds_per_block) kb->lds_per_cu = kb->lds_per_block;
+    if (kb->n_cu <= 0) kb->n_cu = 1;
+    kb->b_in_lds_mode = env_int("KBFOLLOW_B_IN_LDS", -1);
+    kb->n_entities = n_entities;
+    kb->n_relations = n_relations;
+    kb->n_triples = n_triples;
+    kb->weighted = weight != nullptr;
+    const int32_t piece_seg = std::max(1, env_int("KBFOLLOW_PIECE_LEN", 256));
+    const int32_t piece_rel = std::max(1, env_int("KBFOLLOW_REL_PIECE_LEN", 512));
+    const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
+    {
+      LayoutHost H[3];
+      build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, weight, false, H);
+      const int32_t plen[3] = {piece_seg, piece_seg, piece_rel};
+      for (int k = 0; k < 3; ++k) {
+        kb_status st = build_device_layout(kb, kb->L[k], H[k], plen[k], fan_in, s);
+        if (st != KB_OK) {
+          free_kb(kb);
+          return st;
+        }
+        std::vector<int32_t>().swap(H[k].offsets);
+        std::vector<int32_t>().swap(H[k].col_a);
+        std::vector<int32_t>().swap(H[k].col_b);
+        std::vector<float>().swap(H[k].weight);
+      }
+    }
+    *out = kb;
+    return KB_OK;
+  } catch (const std::bad_alloc &) {
+    if (kb) free_kb(kb);
+    return fail(KB_ENOMEM, "host allocation failed");
+  } catch (...) {
+    if (kb) free_kb(kb);
+    return fail(KB_EINVAL, "unexpected host error");
+  }
+}
+
+void kb_destroy(kb_t *kb) {
+  if (kb) free_kb(kb);
+}
+
+size_t kb_workspace_size(const kb_t *kb, int32_t b) {
+  if (!kb || b < 1) return 0;
+  return workspace_bytes(kb, b);
+}
+
+kb_status kb_get_info(const kb_t *kb, kb_info_t *info) {
+  if (!kb || !info) return fail(KB_EINVAL, "kb and info must be non-NULL");
+  std::memset(info, 0, sizeof *info);
+  info->n_entities = kb->n_entities;
+  info->n_relations = kb->n_relations;
+  info->n_triples = kb->n_triples;
+  info->weighted = kb->weighted ? 1 : 0;
+  for (int k = 0; k < 3; ++k) {
+    const DevLayout &D = kb->L[k];
+    info->piece_len[k] = D.piece_len;
+    info->n_pieces[k] = D.n_pieces;
+    info->n_split_rows[k] = D.n_split_rows;
+    info->n_slots[k] = D.n_slots;
+    info->n_levels[k] = (int32_t)D.level_begin.size() - 1;
+    info->n_empty_rows[k] = D.n_empty;
+    info->max_row_len[k] = D.max_row_len;
+  }
+  info->device_bytes = kb->device_bytes;
+  return KB_OK;
+}
+
+kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, float *Y,
+                    void *workspace, size_t ws_bytes, void *stream) {
+  try {
+    if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
+    if (b < 1) return fail(KB_EINVAL, "b must be >= 1");
+    const size_t ent_bytes = (size_t)kb->n_entities * b * sizeof(float);
+    const size_t rel_bytes = (size_t)kb->n_relations * b * sizeof(float);
+    if ((ent_bytes && (!X || !Y)) || (rel_bytes && !R))
+      return fail(KB_EINVAL, "X, R and Y must be non-NULL");
+    const size_t al = (b % 4 == 0) ? 16 : 4;
+    if ((X && !aligned(X, al)) || (R && !aligned(R, al)) || (Y && !aligned(Y, al)))
+      return fail(KB_EINVAL, "X, R and Y must be " + std::to_string(al) + "-byte aligned");
+    if (overlaps(Y, ent_bytes, X, ent_bytes) || overlaps(Y, ent_bytes, R, rel_bytes))
+      return fail(KB_EINVAL, "Y overlaps X or R");
+    kb_status st = check_ws(kb, b, workspace, ws_bytes);
+    if (st != KB_OK) return st;
+    if ((st = check_device(kb)) != KB_OK) return st;
+    g_last_error.clear();
+    if (!ent_bytes) return KB_OK;
+    return run_pass(kb, kb->L[BY_OBJ], KB_PH_FWD_PIECES, X, R, kb->n_relations, true, b, Y,
+                    workspace, static_cast<hipStream_t>(stream));
+  } catch (...) {
+    return fail(KB_EINVAL, "unexpected host error");
+  }
+}
+
+kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const float *R,
+                             const float *dY, float *dX, float *dR, void *workspace,
+                             size_t ws_bytes, void *stream) {
+  try {
+    if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
+    if (b < 1) return fail(KB_EINVAL, "b must be >= 1");
+    const size_t ent_bytes = (size_t)kb->n_entities * b * sizeof(float);
+    const size_t rel_bytes = (size_t)kb->n_relations * b * sizeof(float);
+    const bool want_dx = dX != nullptr && ent_bytes > 0;
+    const bool want_dr = dR != nullptr && rel_bytes > 0;
+    if ((want_dx || want_dr) && ent_bytes && !dY) return fail(KB_EINVAL, "dY must be non-NULL");
+    if (want_dx && rel_bytes && !R) return fail(KB_EINVAL, "R must be non-NULL to compute dX");
+    if (want_dr && ent_bytes && !X) return fail(KB_EINVAL, "X must be non-NULL to compute dR");
+    const size_t al = (b % 4 == 0) ? 16 : 4;
+    for (const void *p : {(const void *)X, (const void *)R, (const void *)dY, (const void *)dX,
+                          (const void *)dR})
+      if (p && !aligned(p, al))
+        return fail(KB_EINVAL, "arrays must be " + std::to_string(al) + "-byte aligned");
+    if (want_dx && (overlaps(dX, ent_bytes, X, ent_bytes) || overlaps(dX, ent_bytes, R, rel_bytes) ||
+                    overlaps(dX, ent_bytes, dY, ent_bytes) || overlaps(dX, ent_bytes, dR, rel_bytes)))
+      return fail(KB_EINVAL, "dX overlaps another array");
+    if (want_dr && (overlaps(dR, rel_bytes, X, ent_bytes) || overlaps(dR, rel_bytes, R, rel_bytes) ||
+                    overlaps(dR, rel_bytes, dY, ent_bytes)))
+      return fail(KB_EINVAL, "dR overlaps another array");
+    kb_status st = check_ws(kb, b, workspace, ws_bytes);
+    if (st != KB_OK) return st;
+    if ((st = check_device(kb)) != KB_OK) return st;
+    g_last_error.clear();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (want_dx) {
+      st = run_pass(kb, kb->L[BY_SUBJ], KB_PH_DX_PIECES, dY, R, kb->n_relations, true, b, dX,
+                    workspace, s);
+      if (st != KB_OK) return st;
+    }
+    if (want_dr) {
+      st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_PIECES, X, dY, kb->n_entities, false, b, dR,
+                    workspace, s);
+      if (st != KB_OK) return st;
+    }
+    return KB_OK;
+  } catch (...) {
+    return fail(KB_EINVAL, "unexpected host error");
+  }
+}
+
+kb_status kb_profile_enable(kb_t *kb, int32_t on) {
+  if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
+  kb_status st = kb_profile_read(kb, nullptr, nullptr);
+  if (st != KB_OK) return st;
+  kb->timing.on = on != 0;
+  return KB_OK;
+}
+
+kb_status kb_profile_read(kb_t *kb, double *ms, int64_t *launches) {
+  if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
+  Timing &t = kb->timing;
+  kb_status st = KB_OK;
+  for (auto &r : t.recs) {
+    hipError_t e = hipEventSynchronize(r.stop);
+    float el = 0.0f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&el, r.start, r.stop);
+    if (e != hipSuccess && st == KB_OK) st = hip_fail(e, "hipEventElapsedTime");
+    if (ms) ms[r.phase] += el;
+    if (launches) ++launches[r.phase];
+    t.pool.push_back(r.start);
+    t.pool.push_back(r.stop);
+  }
+  t.recs.clear();
+  return st;
+}
+
+}  // extern "C"

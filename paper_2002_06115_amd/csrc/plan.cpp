@@ -1,0 +1,164 @@
+// plan.cpp -- host-side layouts and work plans of a reified KB.
+//
+// The reified KB of Sec. 2.3 keeps, per triple, its subject, object and
+// relation ids (the one nonzero of row l in M_subj, M_obj and M_rel).  Here
+// the triples are sorted three ways with stable counting sorts (O(N_T + N)
+// each): by (s, o, r), by (o, s, r) and by (r, s, o).  The secondary keys put
+// equal gathered ids next to each other inside a row, so repeated rows of X or
+// dY are read back to back.
+#include "plan.h"
+
+#include <algorithm>
+#include <cstdio>
+
+namespace kbf {
+
+std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_triples,
+                             const int32_t *subj, const int32_t *rel, const int32_t *obj,
+                             bool *range_error) {
+  *range_error = false;
+  char msg[160];
+  if (n_entities < 0 || n_relations < 0 || n_triples < 0)
+    return "n_entities, n_relations and n_triples must be >= 0";
+  if (n_entities > INT32_MAX || n_relations > INT32_MAX)
+    return "n_entities and n_relations must be below 2^31";
+  if (n_triples > INT32_MAX) return "n_triples must be below 2^31";
+  if (n_triples > 0 && (!subj || !rel || !obj)) return "subj, rel and obj must be non-NULL";
+  for (int64_t l = 0; l < n_triples; ++l) {
+    if (subj[l] < 0 || subj[l] >= n_entities || obj[l] < 0 || obj[l] >= n_entities ||
+        rel[l] < 0 || rel[l] >= n_relations) {
+      *range_error = true;
+      std::snprintf(msg, sizeof msg, "triple %lld = (%d, %d, %d) has an id out of range",
+                    (long long)l, subj[l], rel[l], obj[l]);
+      return msg;
+    }
+  }
+  return "";
+}
+
+// Stable counting sort of the triple ids in `in` by key[id], key in [0, n_keys).
+static void counting_sort(const int32_t *key, int64_t n_keys, const std::vector<int32_t> &in,
+                          std::vector<int32_t> &out, std::vector<int32_t> *offsets) {
+  std::vector<int64_t> start(n_keys + 1, 0);
+  for (int32_t id : in) ++start[key[id] + 1];
+  for (int64_t k = 0; k < n_keys; ++k) start[k + 1] += start[k];
+  if (offsets) {
+    offsets->resize(n_keys + 1);
+    for (int64_t k = 0; k <= n_keys; ++k) (*offsets)[k] = (int32_t)start[k];
+  }
+  out.resize(in.size());
+  for (int32_t id : in) out[start[key[id]]++] = id;
+}
+
+static void fill_layout(LayoutHost &L, int64_t rows, std::vector<int32_t> &&order,
+                        std::vector<int32_t> &&offsets, const int32_t *a, const int32_t *b,
+                        const float *weight, bool keep_perm) {
+  L.rows = rows;
+  L.offsets = std::move(offsets);
+  const size_t n = order.size();
+  L.col_a.resize(n);
+  L.col_b.resize(n);
+  for (size_t p = 0; p < n; ++p) {
+    L.col_a[p] = a[order[p]];
+    L.col_b[p] = b[order[p]];
+  }
+  if (weight) {
+    L.weight.resize(n);
+    for (size_t p = 0; p < n; ++p) L.weight[p] = weight[order[p]];
+  }
+  if (keep_perm) L.perm = std::move(order);
+}
+
+void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
+                   const int32_t *subj, const int32_t *rel, const int32_t *obj,
+                   const float *weight, bool keep_perm, LayoutHost out[3]) {
+  std::vector<int32_t> ident(n_triples), t1, t2, by_subj, by_obj, by_rel;
+  for (int64_t l = 0; l < n_triples; ++l) ident[l] = (int32_t)l;
+  std::vector<int32_t> off_subj, off_obj, off_rel;
+  // (s, o, r): least significant key first.
+  counting_sort(rel, n_relations, ident, t1, nullptr);
+  counting_sort(obj, n_entities, t1, t2, nullptr);
+  counting_sort(subj, n_entities, t2, by_subj, &off_subj);
+  std::vector<int32_t>().swap(ident);
+  std::vector<int32_t>().swap(t1);
+  std::vector<int32_t>().swap(t2);
+  // (o, s, r) and (r, s, o) from the (s, o, r) order.
+  counting_sort(obj, n_entities, by_subj, by_obj, &off_obj);
+  counting_sort(rel, n_relations, by_subj, by_rel, &off_rel);
+  fill_layout(out[BY_OBJ], n_entities, std::move(by_obj), std::move(off_obj), subj, rel, weight,
+              keep_perm);
+  fill_layout(out[BY_SUBJ], n_entities, std::move(by_subj), std::move(off_subj), obj, rel,
+              weight, keep_perm);
+  fill_layout(out[BY_REL], n_relations, std::move(by_rel), std::move(off_rel), subj, obj, weight,
+              keep_perm);
+}
+
+PlanHost plan_layout(const LayoutHost &L, int32_t piece_len, int32_t fan_in) {
+  PlanHost P;
+  P.piece_len = piece_len;
+  P.fan_in = fan_in;
+  struct Split {
+    int32_t row;
+    int64_t first, n;
+  };
+  std::vector<Split> splits;
+  std::vector<Piece> raw;
+  std::vector<int64_t> count_by_len(piece_len + 1, 0);
+  for (int64_t q = 0; q < L.rows; ++q) {
+    const int64_t beg = L.offsets[q], deg = L.offsets[q + 1] - beg;
+    P.max_row_len = std::max(P.max_row_len, deg);
+    if (deg == 0) {
+      P.empty_rows.push_back((int32_t)q);
+    } else if (deg <= piece_len) {
+      raw.push_back({(int32_t)beg, (int32_t)deg, (int32_t)q, 0});
+      ++count_by_len[deg];
+    } else {
+      const int64_t np = (deg + piece_len - 1) / piece_len;
+      splits.push_back({(int32_t)q, P.n_slots, np});
+      for (int64_t k = 0; k < np; ++k) {
+        const int32_t len = (int32_t)std::min<int64_t>(piece_len, deg - k * piece_len);
+        raw.push_back({(int32_t)(beg + k * piece_len), len, (int32_t)(-(P.n_slots + k) - 1), 0});
+        ++count_by_len[len];
+      }
+      P.n_slots += np;
+      ++P.n_split_rows;
+    }
+  }
+  // Longest pieces first (stable within a length): lane groups of one
+  // wavefront then get pieces of equal or similar length.
+  std::vector<int64_t> first(piece_len + 1, 0);
+  {
+    int64_t acc = 0;
+    for (int32_t len = piece_len; len >= 1; --len) {
+      first[len] = acc;
+      acc += count_by_len[len];
+    }
+  }
+  P.pieces.resize(raw.size());
+  for (const Piece &p : raw) P.pieces[first[p.len]++] = p;
+  // Combine levels: a row split into n pieces is reduced fan_in slots at a
+  // time until one task writes the row.
+  for (const Split &s : splits) {
+    int64_t first_slot = s.first, n = s.n;
+    size_t level = 0;
+    while (n > fan_in) {
+      const int64_t groups = (n + fan_in - 1) / fan_in;
+      const int64_t out0 = P.n_slots;
+      P.n_slots += groups;
+      if (P.levels.size() <= level) P.levels.resize(level + 1);
+      for (int64_t g = 0; g < groups; ++g) {
+        const int64_t cnt = std::min<int64_t>(fan_in, n - g * fan_in);
+        P.levels[level].push_back({(int32_t)(first_slot + g * fan_in), (int32_t)cnt,
+                                   (int32_t)(-(out0 + g) - 1), 0});
+      }
+      first_slot = out0;
+      n = groups;
+      ++level;
+    }
+    if (P.levels.size() <= level) P.levels.resize(level + 1);
+    P.levels[level].push_back({(int32_t)first_slot, (int32_t)n, s.row, 0});
+  }
+  return P;
+}
+
+}  // namespace kbf

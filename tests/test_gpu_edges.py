@@ -1,0 +1,128 @@
+"""GPU edge cases against the oracle: empty KB, odd batch sizes, one-hub KBs,
+a single relation, a single entity with duplicate self-loops, empty rows next
+to 2^20-triple rows, and argument errors."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import assert_bitexact, assert_close, from_em, to_em
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kbf():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2002_06115_amd as kbf
+    return kbf
+
+
+def both(kbf, s, r, o, n_e, n_r, X, R, dY, exact, label, weight=None):
+    print(f"[edge] {label} NE={n_e} NR={n_r} NT={len(s)} b={X.shape[0]}", flush=True)
+    kb = kbf.KB(s, r, o, n_e, n_r, weight=weight)
+    Y = from_em(kb.follow(to_em(X), to_em(R)))
+    dX, dR = kb.follow_backward(to_em(X), to_em(R), to_em(dY))
+    got = (Y, from_em(dX), from_em(dR))
+    Yo = oracle.follow(s, r, o, n_e, n_r, X, R, weight=weight)
+    dXo, dRo = oracle.follow_backward(s, r, o, n_e, n_r, X, R, dY, weight=weight)
+    for name, g, e in zip(("Y", "dX", "dR"), got, (Yo, dXo, dRo)):
+        (assert_bitexact if exact else assert_close)(g, e, f"{label} {name}")
+    return kb
+
+
+def rand_kb(seed, n_e, n_r, n_t):
+    g = np.random.default_rng(seed)
+    return (g.integers(0, n_e, n_t).astype(np.int32), g.integers(0, n_r, n_t).astype(np.int32),
+            g.integers(0, n_e, n_t).astype(np.int32))
+
+
+def rand_io(seed, b, n_e, n_r):
+    g = np.random.default_rng(seed)
+    return (g.standard_normal((b, n_e)).astype(np.float32), g.standard_normal((b, n_r)).astype(np.float32),
+            g.standard_normal((b, n_e)).astype(np.float32))
+
+
+@pytest.mark.parametrize("b", [1, 2, 3, 4, 5, 8, 12, 33, 64, 100, 260, 300, 513])
+def test_batch_sizes(kbf, b):
+    n_e, n_r = 700, 6
+    s, r, o = rand_kb(b, n_e, n_r, 6000)
+    X, R, dY = rand_io(b, b, n_e, n_r)
+    both(kbf, s, r, o, n_e, n_r, X, R, dY, False, f"b={b}")
+
+
+def test_empty_kb(kbf):
+    e = np.zeros(0, np.int32)
+    X, R, dY = rand_io(1, 4, 50, 3)
+    both(kbf, e, e, e, 50, 3, X, R, dY, True, "empty")
+
+
+def test_one_hub_holds_every_triple(kbf):
+    n_e, n_r, n_t = 20_000, 4, 300_000
+    g = np.random.default_rng(2)
+    s = np.full(n_t, 17, np.int32)
+    r = g.integers(0, n_r, n_t).astype(np.int32)
+    o = g.integers(0, n_e, n_t).astype(np.int32)
+    X, R, dY = rand_io(2, 32, n_e, n_r)
+    both(kbf, s, r, o, n_e, n_r, X, R, dY, False, "subject hub")
+    both(kbf, o, r, s, n_e, n_r, X, R, dY, False, "object hub")
+
+
+def test_single_relation(kbf):
+    s, r, o = rand_kb(3, 5000, 1, 40_000)
+    X, R, dY = rand_io(3, 16, 5000, 1)
+    both(kbf, s, r, o, 5000, 1, X, R, dY, False, "N_R=1")
+
+
+def test_single_entity_duplicate_self_loops(kbf):
+    n_t = 5000
+    s = np.zeros(n_t, np.int32)
+    r = (np.arange(n_t) % 3).astype(np.int32)
+    X = np.full((8, 1), 1.0, np.float32)
+    R = np.ones((8, 3), np.float32)
+    dY = np.ones((8, 1), np.float32)
+    both(kbf, s, r, s, 1, 3, X, R, dY, True, "N_E=1 duplicates")
+
+
+def test_empty_rows_beside_huge_rows(kbf):
+    # Two rows of 2^20 triples (several combine levels), the rest mostly empty.
+    n_e, n_r = 50_000, 5
+    g = np.random.default_rng(4)
+    big = 1 << 20
+    s = np.concatenate([np.full(big, 11), np.full(big, 40_000), g.integers(0, 100, 5000)]).astype(np.int32)
+    o = np.concatenate([g.integers(0, 30, big), g.integers(0, n_e, big), np.full(5000, 7)]).astype(np.int32)
+    r = g.integers(0, n_r, len(s)).astype(np.int32)
+    Xi = (g.random((4, n_e)) < 0.3).astype(np.float32)
+    Ri = np.zeros((4, n_r), np.float32)
+    Ri[np.arange(4), g.integers(0, n_r, 4)] = 1.0
+    both(kbf, s, r, o, n_e, n_r, Xi, Ri, np.ones((4, n_e), np.float32), True, "hubs+empty int")
+    X, R, dY = rand_io(4, 32, n_e, n_r)
+    kb = both(kbf, s, r, o, n_e, n_r, X, R, dY, False, "hubs+empty real")
+    info = kb.info()
+    assert max(info["n_levels"]) >= 2 and info["n_empty_rows"][0] > 0
+
+
+def test_argument_errors(kbf):
+    import torch
+    s, r, o = rand_kb(5, 100, 3, 2000)
+    kb = kbf.KB(s, r, o, 100, 3)
+    X = torch.zeros((100, 8), device="cuda")
+    R = torch.zeros((3, 8), device="cuda")
+    lib = kbf._lib
+    h = kb._handle
+    p = lambda t: ctypes.c_void_p(t.data_ptr())
+    ws = kb.workspace(8)
+    nws = 0 if ws is None else ws.numel()
+    wsp = None if ws is None else p(ws)
+    assert lib.kb_follow(h, 0, p(X), p(R), p(X), wsp, nws, None) == kbf.KB_EINVAL       # b < 1
+    assert lib.kb_follow(h, 8, p(X), p(R), p(X), wsp, nws, None) == kbf.KB_EINVAL       # Y aliases X
+    assert lib.kb_follow(h, 8, None, p(R), p(X), wsp, nws, None) == kbf.KB_EINVAL       # NULL X
+    Xo = torch.zeros(100 * 8 + 1, device="cuda")[1:].view(100, 8)
+    Y = torch.zeros((100, 8), device="cuda")
+    assert lib.kb_follow(h, 8, p(Xo), p(R), p(Y), wsp, nws, None) == kbf.KB_EINVAL      # misaligned
+    torch.cuda.synchronize()
+    with pytest.raises(ValueError):
+        kb.follow(X, torch.zeros((3, 7), device="cuda"))
