@@ -27,9 +27,9 @@ sys.path.insert(0, ROOT)
 METRIC = "triple·batch products/sec for kb_follow fwd+bwd; achieved HBM GB/s vs peak"
 PEAK_HBM_GBPS = 8000.0
 DOMINANT_KERNEL_NAMES = {
-    "fwd_pieces": "pieces_kernel (forward: objects, gathers X)",
-    "dx_pieces": "pieces_kernel (dX: subjects, gathers dY)",
-    "dr_pieces": "pieces_kernel (dR: relations, gathers X and dY)",
+    "fwd_stream": "stream_kernel (forward: objects, gathers X)",
+    "dx_stream": "stream_kernel (dX: subjects, gathers dY)",
+    "dr_stream": "stream_kernel (dR: relations, gathers X and dY)",
 }
 
 
@@ -38,15 +38,15 @@ def log(*a):
 
 
 def pass_bytes(kb, b, phase):
-    """Algorithmic bytes of one pieces-kernel launch (gather model: every
+    """Algorithmic bytes of one stream-kernel launch (gather model: every
     triple's b-wide operand rows come from memory; plus the index stream and
     the output rows), and the compulsory model (each distinct row once)."""
     n_t, n_e, n_r = kb.n_triples, kb.n_entities, kb.n_relations
     idx = 8 * n_t
-    if phase in ("fwd_pieces", "dx_pieces"):
+    if phase in ("fwd_stream", "dx_stream"):
         gather = idx + 4 * (n_e + 1) + 4 * b * n_t + 4 * b * n_e      # A gathered per triple, R from LDS/L2
-        a_ids = kb.subj if phase == "fwd_pieces" else kb.obj
-        out_ids = kb.obj if phase == "fwd_pieces" else kb.subj
+        a_ids = kb.subj if phase == "fwd_stream" else kb.obj
+        out_ids = kb.obj if phase == "fwd_stream" else kb.subj
         comp = idx + 4 * (n_e + 1) + 4 * b * len(np.unique(a_ids)) + 4 * b * n_r \
             + 4 * b * len(np.unique(out_ids))
     else:
@@ -84,9 +84,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="large",
                     help="tiny | metaqa | large | train (kbgen workload names)")
-    ap.add_argument("--cpu-cols", type=int, default=8, help="batch columns the oracle times")
+    ap.add_argument("--cpu-cols", type=int, default=0,
+                    help="batch columns the oracle times (0 = all b)")
+    ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the HIP-event phase timing")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 5 times (to scale rocprofv3 "
+                         "FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the follow path here has no multi-GPU sharding "
@@ -96,6 +101,17 @@ def main():
     import torch
     import kbgen
     import paper_2002_06115_amd as kbf
+
+    if args.copy_calibration:
+        n = (1 << 30) // 4
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"bytes_read": 4 * n, "bytes_written": 4 * n,
+                                               "launches": 5}}))
+        return
 
     w = kbgen.WORKLOADS[args.workload]
     if w.name == "chain3":
@@ -147,7 +163,7 @@ def main():
 
     roof = None
     if phases:
-        dom = max(("fwd_pieces", "dx_pieces", "dr_pieces"), key=lambda p: phases[p][0])
+        dom = max(("fwd_stream", "dx_stream", "dr_stream"), key=lambda p: phases[p][0])
         ms_avg = phases[dom][0] / max(1, phases[dom][1])
         gather_b, comp_b = pass_bytes(kb, b, dom)
         achieved = gather_b / (ms_avg * 1e-3) / 1e9
@@ -162,8 +178,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cols = max(1, min(args.cpu_cols, b))
-        threads = min(cols, os.cpu_count() or 1)
+        cols = b if args.cpu_cols <= 0 else max(1, min(args.cpu_cols, b))
+        threads = max(1, min(cols, args.cpu_threads, os.cpu_count() or 1))
         log(f"[bench] timing the CPU oracle on {cols} batch columns, {threads} threads")
         cpu = cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads)
         log(f"[bench] oracle {cpu['value']:.3e} triple*batch/s")

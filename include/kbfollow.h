@@ -77,6 +77,8 @@ typedef enum {
  *
  * The three sorted layouts (by object, by subject, by relation) and their
  * work plans are built on the host and uploaded; the host copies are freed.
+ * Device memory held: 16 bytes per triple per layout (48 per triple) plus
+ * small plans.
  * Errors: KB_EINVAL (sizes, null pointers), KB_ERANGE (an id out of range;
  * checked before any device work), KB_ENOMEM, KB_EHIP.
  */
@@ -89,7 +91,7 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
 void kb_destroy(kb_t *kb);
 
 /* Bytes of device workspace that kb_follow and kb_follow_backward need for
- * batch size b (scratch for the partial sums of rows split into pieces).  May
+ * batch size b (scratch for the partial sums of rows that cross chunks).  May
  * be 0.  Returns 0 for a NULL kb or b < 1. */
 size_t kb_workspace_size(const kb_t *kb, int32_t b);
 
@@ -144,9 +146,9 @@ const char *kb_last_error(void);
 typedef struct {
   int64_t n_entities, n_relations, n_triples;
   int32_t weighted;         /* 1 if built with per-triple weights */
-  int32_t piece_len[3];     /* longest piece of a row one lane group sums (obj, subj, rel) */
-  int64_t n_pieces[3];      /* work items per layout: by object, by subject, by relation */
-  int64_t n_split_rows[3];  /* rows cut into more than one piece */
+  int32_t chunk_len[3];     /* triples per chunk, one chunk per lane group (obj, subj, rel) */
+  int64_t n_chunks[3];      /* chunks per layout: by object, by subject, by relation */
+  int64_t n_split_rows[3];  /* rows that cross a chunk boundary */
   int64_t n_slots[3];       /* partial-sum slots (all combine levels) */
   int32_t n_levels[3];      /* combine levels */
   int64_t n_empty_rows[3];  /* rows with no triple (written as zeros) */
@@ -176,9 +178,9 @@ kb_status kb_layout_host(int64_t n_entities, int64_t n_relations, int64_t n_trip
 
 /* Phases whose GPU time is recorded when profiling is on. */
 typedef enum {
-  KB_PH_FWD_PIECES = 0, KB_PH_FWD_COMBINE, KB_PH_FWD_ZERO,
-  KB_PH_DX_PIECES, KB_PH_DX_COMBINE, KB_PH_DX_ZERO,
-  KB_PH_DR_PIECES, KB_PH_DR_COMBINE, KB_PH_DR_ZERO,
+  KB_PH_FWD_STREAM = 0, KB_PH_FWD_COMBINE, KB_PH_FWD_ZERO,
+  KB_PH_DX_STREAM, KB_PH_DX_COMBINE, KB_PH_DX_ZERO,
+  KB_PH_DR_STREAM, KB_PH_DR_COMBINE, KB_PH_DR_ZERO,
   KB_PH_COUNT
 } kb_phase;
 

@@ -26,8 +26,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "_lib", "libkbfollow.so")
 
 KB_OK, KB_EINVAL, KB_ERANGE, KB_ENOMEM, KB_EHIP, KB_ENOTSUP = range(6)
-PHASES = ("fwd_pieces", "fwd_combine", "fwd_zero", "dx_pieces", "dx_combine", "dx_zero",
-          "dr_pieces", "dr_combine", "dr_zero")
+PHASES = ("fwd_stream", "fwd_combine", "fwd_zero", "dx_stream", "dx_combine", "dx_zero",
+          "dr_stream", "dr_combine", "dr_zero")
 
 
 class KBError(RuntimeError):
@@ -39,7 +39,7 @@ class KBError(RuntimeError):
 class KBInfo(ctypes.Structure):
     _fields_ = [("n_entities", ctypes.c_int64), ("n_relations", ctypes.c_int64),
                 ("n_triples", ctypes.c_int64), ("weighted", ctypes.c_int32),
-                ("piece_len", ctypes.c_int32 * 3), ("n_pieces", ctypes.c_int64 * 3),
+                ("chunk_len", ctypes.c_int32 * 3), ("n_chunks", ctypes.c_int64 * 3),
                 ("n_split_rows", ctypes.c_int64 * 3), ("n_slots", ctypes.c_int64 * 3),
                 ("n_levels", ctypes.c_int32 * 3), ("n_empty_rows", ctypes.c_int64 * 3),
                 ("max_row_len", ctypes.c_int64 * 3), ("device_bytes", ctypes.c_int64)]

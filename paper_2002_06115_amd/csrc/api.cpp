@@ -28,13 +28,13 @@ kb_status hip_fail(hipError_t e, const char *what) {
   return fail(KB_EHIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Work plan of one layout, resident on the device.
+// Stream plan of one layout, resident on the device.
 struct DevLayout {
   int64_t rows = 0;
-  int2 *pairs = nullptr;      // (gathered id, second id) per position
-  float *weight = nullptr;    // per position or nullptr
-  int4 *pieces = nullptr;
-  int64_t n_pieces = 0;
+  int4 *entries = nullptr;    // per position: (gathered id, second id, flush, weight bits)
+  int64_t n = 0;
+  int32_t chunk = 0;
+  int64_t n_chunks = 0;
   int32_t *empty = nullptr;
   int64_t n_empty = 0;
   int4 *ctasks = nullptr;     // all combine levels, back to back
@@ -42,7 +42,6 @@ struct DevLayout {
   int64_t n_slots = 0;
   int64_t n_split_rows = 0;
   int64_t max_row_len = 0;
-  int32_t piece_len = 0;
 };
 
 struct Timing {
@@ -108,21 +107,26 @@ void free_kb(kb_t *kb) {
   delete kb;
 }
 
-kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32_t piece_len,
+kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32_t chunk,
                               int32_t fan_in, hipStream_t s) {
-  PlanHost P = plan_layout(H, piece_len, fan_in);
+  PlanHost P = plan_layout(H, chunk, fan_in);
   D.rows = H.rows;
-  D.piece_len = piece_len;
-  D.n_pieces = (int64_t)P.pieces.size();
+  D.n = (int64_t)H.col_a.size();
+  D.chunk = chunk;
+  D.n_chunks = P.n_chunks;
   D.n_empty = (int64_t)P.empty_rows.size();
   D.n_slots = P.n_slots;
   D.n_split_rows = P.n_split_rows;
   D.max_row_len = P.max_row_len;
-  std::vector<int2> pairs(H.col_a.size());
-  for (size_t p = 0; p < pairs.size(); ++p) pairs[p] = make_int2(H.col_a[p], H.col_b[p]);
-  std::vector<int4> pieces(P.pieces.size());
-  for (size_t i = 0; i < pieces.size(); ++i)
-    pieces[i] = make_int4(P.pieces[i].start, P.pieces[i].len, P.pieces[i].dst, 0);
+  std::vector<int4> entries(D.n);
+  const bool wt = !H.weight.empty();
+  for (int64_t p = 0; p < D.n; ++p) {
+    float w = wt ? H.weight[p] : 1.0f;
+    int32_t wbits;
+    std::memcpy(&wbits, &w, sizeof wbits);
+    entries[p] = make_int4(H.col_a[p], H.col_b[p], P.flush[p], wbits);
+  }
+  std::vector<int32_t>().swap(P.flush);
   std::vector<int4> ctasks;
   D.level_begin.assign(1, 0);
   for (const auto &lv : P.levels) {
@@ -130,9 +134,7 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
     D.level_begin.push_back((int64_t)ctasks.size());
   }
   kb_status st;
-  if ((st = upload(kb, pairs, &D.pairs, s)) != KB_OK) return st;
-  if ((st = upload(kb, H.weight, &D.weight, s)) != KB_OK) return st;
-  if ((st = upload(kb, pieces, &D.pieces, s)) != KB_OK) return st;
+  if ((st = upload(kb, entries, &D.entries, s)) != KB_OK) return st;
   if ((st = upload(kb, P.empty_rows, &D.empty, s)) != KB_OK) return st;
   if ((st = upload(kb, ctasks, &D.ctasks, s)) != KB_OK) return st;
   // The host vectors die with this frame: wait for the copies first.
@@ -188,31 +190,33 @@ kb_status check_device(const kb_t *kb) {
   return KB_OK;
 }
 
-// Runs one pass: pieces, combine levels, empty rows.
+// Runs one pass: the stream kernel, the combine levels, the empty rows.
 kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float *A,
                    const float *B, int64_t B_rows, bool b_may_use_lds, int32_t b, float *out,
                    void *ws, hipStream_t s) {
   double *slots = static_cast<double *>(ws);
   {
     PhaseScope scope(kb, ph_base + 0, s);
-    PiecesArgs a{D.pieces, D.n_pieces, D.pairs, D.weight, A, B, B_rows, b, out, slots};
+    StreamArgs a{D.entries, D.n, D.chunk, A, B, B_rows, b, out, slots};
     bool lds = false;
     int max_blocks = 0;
     if (b_may_use_lds && kb->b_in_lds_mode != 0) {
-      const size_t bytes = pieces_lds_bytes(b, B_rows);
-      const size_t limit = kb->b_in_lds_mode == 1 ? kb->lds_per_block : std::min<size_t>(kb->lds_per_block, 64 * 1024);
+      const size_t bytes = stream_lds_bytes(b, B_rows);
+      const size_t limit = kb->b_in_lds_mode == 1
+                               ? kb->lds_per_block
+                               : std::min<size_t>(kb->lds_per_block, 64 * 1024);
       if (bytes > 0 && bytes <= limit) {
         lds = true;
         const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(8, kb->lds_per_cu / bytes));
         max_blocks = kb->n_cu * per_cu;
         if (bytes > 64 * 1024) {
-          hipError_t e = prepare_pieces_lds(b, bytes);
+          hipError_t e = prepare_stream_lds(b, bytes);
           if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
         }
       }
     }
-    hipError_t e = launch_pieces(a, lds, max_blocks, s);
-    if (e != hipSuccess) return hip_fail(e, "pieces kernel launch");
+    hipError_t e = launch_stream(a, kb->weighted, lds, max_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
   {
     PhaseScope scope(kb, ph_base + 1, s);
@@ -323,13 +327,13 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     kb->n_relations = n_relations;
     kb->n_triples = n_triples;
     kb->weighted = weight != nullptr;
-    const int32_t piece_seg = std::max(1, env_int("KBFOLLOW_PIECE_LEN", 256));
-    const int32_t piece_rel = std::max(1, env_int("KBFOLLOW_REL_PIECE_LEN", 512));
+    const int32_t chunk_seg = std::max(1, env_int("KBFOLLOW_CHUNK", 256));
+    const int32_t chunk_rel = std::max(1, env_int("KBFOLLOW_REL_CHUNK", 256));
     const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
     {
       LayoutHost H[3];
       build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, weight, false, H);
-      const int32_t plen[3] = {piece_seg, piece_seg, piece_rel};
+      const int32_t plen[3] = {chunk_seg, chunk_seg, chunk_rel};
       for (int k = 0; k < 3; ++k) {
         kb_status st = build_device_layout(kb, kb->L[k], H[k], plen[k], fan_in, s);
         if (st != KB_OK) {
@@ -371,8 +375,8 @@ kb_status kb_get_info(const kb_t *kb, kb_info_t *info) {
   info->weighted = kb->weighted ? 1 : 0;
   for (int k = 0; k < 3; ++k) {
     const DevLayout &D = kb->L[k];
-    info->piece_len[k] = D.piece_len;
-    info->n_pieces[k] = D.n_pieces;
+    info->chunk_len[k] = D.chunk;
+    info->n_chunks[k] = D.n_chunks;
     info->n_split_rows[k] = D.n_split_rows;
     info->n_slots[k] = D.n_slots;
     info->n_levels[k] = (int32_t)D.level_begin.size() - 1;
@@ -402,7 +406,7 @@ kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, f
     if ((st = check_device(kb)) != KB_OK) return st;
     g_last_error.clear();
     if (!ent_bytes) return KB_OK;
-    return run_pass(kb, kb->L[BY_OBJ], KB_PH_FWD_PIECES, X, R, kb->n_relations, true, b, Y,
+    return run_pass(kb, kb->L[BY_OBJ], KB_PH_FWD_STREAM, X, R, kb->n_relations, true, b, Y,
                     workspace, static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(KB_EINVAL, "unexpected host error");
@@ -439,12 +443,12 @@ kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const fl
     g_last_error.clear();
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (want_dx) {
-      st = run_pass(kb, kb->L[BY_SUBJ], KB_PH_DX_PIECES, dY, R, kb->n_relations, true, b, dX,
+      st = run_pass(kb, kb->L[BY_SUBJ], KB_PH_DX_STREAM, dY, R, kb->n_relations, true, b, dX,
                     workspace, s);
       if (st != KB_OK) return st;
     }
     if (want_dr) {
-      st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_PIECES, X, dY, kb->n_entities, false, b, dR,
+      st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_STREAM, X, dY, kb->n_entities, false, b, dR,
                     workspace, s);
       if (st != KB_OK) return st;
     }

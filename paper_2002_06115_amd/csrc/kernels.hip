@@ -14,13 +14,14 @@
 // Activations are entity-major and batch-contiguous ([N][b] float32), so each
 // gather is one contiguous b-wide row: a lane group of LPT lanes reads it with
 // VEC-float (16-byte when VEC = 4) loads, lane l owning columns
-// [col0 + l*VEC, col0 + l*VEC + VEC).  A lane group owns a whole piece (at
-// most a few hundred triples of one row), so a row sum needs no cross-lane
-// reduction at all: every lane accumulates its own columns.  Rows longer than
-// a piece write double partials to workspace slots that the combine kernel
-// adds up in piece order.  No atomics anywhere: every output element is
-// written by exactly one lane, with a fixed summation order, so results are
-// bitwise reproducible.
+// [col0 + l*VEC, col0 + l*VEC + VEC).  The sorted triple list is cut into
+// equal chunks and a lane group walks one chunk sequentially, so a row sum
+// needs no cross-lane reduction at all: every lane accumulates its own
+// columns and writes them when the row ends.  A row that crosses a chunk
+// boundary writes one double partial per chunk to a workspace slot and the
+// combine kernel adds them up in chunk order.  No atomics anywhere: every
+// output element is written by exactly one lane, with a fixed summation
+// order, so results are bitwise reproducible.
 //
 // Arithmetic: each product w * a * b is formed in double (the product of two
 // floats is exact in double) and accumulated in double; the float output is
@@ -28,6 +29,8 @@
 // rows per triple against two flops per element), so the double arithmetic
 // costs no time while it keeps long Zipf-hub rows accurate.
 #include "kernels.h"
+
+#include <climits>
 
 namespace kbf {
 
@@ -83,12 +86,13 @@ __device__ __forceinline__ void store_slot(double *__restrict__ p, const double 
   }
 }
 
-// One lane group (LPT lanes) per piece; pieces are visited grid-stride so a
-// capped (persistent) grid works too.  With B_IN_LDS the workgroup first
-// copies B's column slice [B_rows][W] into LDS (the relation table R is tiny:
-// N_R x b floats) and every triple then reads its B row from LDS.
-template <int VEC, int LPT, bool B_IN_LDS>
-__global__ __launch_bounds__(kBlock) void pieces_kernel(PiecesArgs a) {
+// One lane group (LPT lanes) per chunk of the sorted triple stream; chunks
+// are visited grid-stride so a capped (persistent) grid works too.  Every
+// chunk holds the same number of positions, so the work is balanced whatever
+// the row lengths.  With B_IN_LDS the workgroup first copies B's column slice
+// [B_rows][W] into LDS (the relation table R is tiny: N_R x b floats).
+template <int VEC, int LPT, bool B_IN_LDS, bool WEIGHTED>
+__global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
   extern __shared__ float lds_b[];
@@ -109,52 +113,64 @@ __global__ __launch_bounds__(kBlock) void pieces_kernel(PiecesArgs a) {
     __syncthreads();
   }
 
+  // Loads never sit behind a branch, so all kUnroll gathers of a step are in
+  // flight together: lanes past b read column 0 and store nothing, and the
+  // step past the end of a chunk re-reads its last position and adds nothing.
+  const int cl = active ? c : 0;
+  const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
   const int64_t stride = (int64_t)gridDim.x * GPB;
-  for (int64_t t = (int64_t)blockIdx.x * GPB + grp; t < a.n_pieces; t += stride) {
-    const int4 pc = a.pieces[t];  // start, len, dst
+  for (int64_t g = (int64_t)blockIdx.x * GPB + grp; g < n_chunks; g += stride) {
+    const int64_t p0 = g * a.chunk;
+    const int64_t p1 = min(p0 + (int64_t)a.chunk, a.n);
     double acc[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] = 0.0;
 
-    for (int i = 0; i < pc.y; i += kUnroll) {
-      const int n = min(kUnroll, pc.y - i);
-      int2 id[kUnroll];
-      float w[kUnroll];
+    // Software pipeline: the entries of the next step are loaded while this
+    // step's gathers are in flight.
+    int4 e_next[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) e_next[u] = a.entries[min(p0 + u, p1 - 1)];
+    for (int64_t p = p0; p < p1; p += kUnroll) {
+      const int cnt = (int)min((int64_t)kUnroll, p1 - p);
+      int4 e[kUnroll];
       float xa[kUnroll][VEC], xb[kUnroll][VEC];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        if (u < n) {
-          id[u] = a.pairs[pc.x + i + u];
-          w[u] = a.weight ? a.weight[pc.x + i + u] : 1.0f;
-        }
-      }
+      for (int u = 0; u < kUnroll; ++u) e[u] = e_next[u];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        if (u < n && active) {
-          load_row<VEC>(a.A + (size_t)id[u].x * bb + c, xa[u]);
-          if constexpr (B_IN_LDS)
-            load_row<VEC>(lds_b + (size_t)id[u].y * W + lane * VEC, xb[u]);
-          else
-            load_row<VEC>(a.B + (size_t)id[u].y * bb + c, xb[u]);
-        } else {
-#pragma unroll
-          for (int v = 0; v < VEC; ++v) xa[u][v] = xb[u][v] = 0.0f;
-        }
+        load_row<VEC>(a.A + (size_t)e[u].x * bb + cl, xa[u]);
+        if constexpr (B_IN_LDS)
+          load_row<VEC>(lds_b + (size_t)e[u].y * W + lane * VEC, xb[u]);
+        else
+          load_row<VEC>(a.B + (size_t)e[u].y * bb + cl, xb[u]);
       }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) e_next[u] = a.entries[min(p + kUnroll + u, p1 - 1)];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        if (u < n) {
+        if (u < cnt) {
+          if constexpr (WEIGHTED) {
+            const double w = (double)__int_as_float(e[u].w);
 #pragma unroll
-          for (int v = 0; v < VEC; ++v)
-            acc[v] += (double)w[u] * (double)xa[u][v] * (double)xb[u][v];
+            for (int v = 0; v < VEC; ++v) acc[v] += w * (double)xa[u][v] * (double)xb[u][v];
+          } else {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) acc[v] += (double)xa[u][v] * (double)xb[u][v];
+          }
+          const int f = e[u].z;
+          if (f != INT_MIN) {
+            if (active) {
+              if (f >= 0)
+                store_row<VEC>(a.out + (size_t)f * bb + c, acc);
+              else
+                store_slot<VEC>(a.slots + (size_t)(-(f + 1)) * bb + c, acc);
+            }
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) acc[v] = 0.0;
+          }
         }
       }
-    }
-    if (active) {
-      if (pc.z >= 0)
-        store_row<VEC>(a.out + (size_t)pc.z * bb + c, acc);
-      else
-        store_slot<VEC>(a.slots + (size_t)(-(pc.z + 1)) * bb + c, acc);
     }
   }
 }
@@ -184,7 +200,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
       double part[kUnroll][VEC];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
-        if (u < n) load_slot<VEC>(slots + (size_t)(tk.x + i + u) * bb + c, part[u]);
+        load_slot<VEC>(slots + (size_t)(tk.x + i + min(u, n - 1)) * bb + c, part[u]);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
         if (u < n) {
@@ -217,18 +233,27 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__rest
   }
 }
 
-template <int VEC, bool LDS>
-const void *pieces_fn(int lpt) {
+template <int VEC, bool LDS, bool WT>
+const void *stream_fn(int lpt) {
   switch (lpt) {
-    case 1: return reinterpret_cast<const void *>(&pieces_kernel<VEC, 1, LDS>);
-    case 2: return reinterpret_cast<const void *>(&pieces_kernel<VEC, 2, LDS>);
-    case 4: return reinterpret_cast<const void *>(&pieces_kernel<VEC, 4, LDS>);
-    case 8: return reinterpret_cast<const void *>(&pieces_kernel<VEC, 8, LDS>);
-    case 16: return reinterpret_cast<const void *>(&pieces_kernel<VEC, 16, LDS>);
-    case 32: return reinterpret_cast<const void *>(&pieces_kernel<VEC, 32, LDS>);
-    case 64: return reinterpret_cast<const void *>(&pieces_kernel<VEC, 64, LDS>);
+    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, LDS, WT>);
+    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, LDS, WT>);
+    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, LDS, WT>);
+    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, LDS, WT>);
+    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, LDS, WT>);
+    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, LDS, WT>);
+    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, LDS, WT>);
   }
   return nullptr;
+}
+
+const void *stream_fn_for(const ColumnTiling &t, bool lds, bool wt) {
+  if (t.vec == 4) {
+    if (lds) return wt ? stream_fn<4, true, true>(t.lpt) : stream_fn<4, true, false>(t.lpt);
+    return wt ? stream_fn<4, false, true>(t.lpt) : stream_fn<4, false, false>(t.lpt);
+  }
+  if (lds) return wt ? stream_fn<1, true, true>(t.lpt) : stream_fn<1, true, false>(t.lpt);
+  return wt ? stream_fn<1, false, true>(t.lpt) : stream_fn<1, false, false>(t.lpt);
 }
 
 template <int VEC>
@@ -266,28 +291,33 @@ ColumnTiling column_tiling(int32_t b) {
   return t;
 }
 
-size_t pieces_lds_bytes(int32_t b, int64_t B_rows) {
+size_t stream_lds_bytes(int32_t b, int64_t B_rows) {
   const ColumnTiling t = column_tiling(b);
   return (size_t)B_rows * (size_t)t.width * sizeof(float);
 }
 
-hipError_t prepare_pieces_lds(int32_t b, size_t bytes) {
+hipError_t prepare_stream_lds(int32_t b, size_t bytes) {
   const ColumnTiling t = column_tiling(b);
-  const void *fn = t.vec == 4 ? pieces_fn<4, true>(t.lpt) : pieces_fn<1, true>(t.lpt);
-  if (!fn) return hipErrorInvalidValue;
-  return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  for (bool wt : {false, true}) {
+    const void *fn = stream_fn_for(t, true, wt);
+    if (!fn) return hipErrorInvalidValue;
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
-hipError_t launch_pieces(const PiecesArgs &a, bool b_in_lds, int max_blocks, hipStream_t s) {
-  if (a.n_pieces == 0) return hipSuccess;
+hipError_t launch_stream(const StreamArgs &a, bool weighted, bool b_in_lds, int max_blocks,
+                         hipStream_t s) {
+  if (a.n == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(a.b);
-  const void *fn = t.vec == 4 ? (b_in_lds ? pieces_fn<4, true>(t.lpt) : pieces_fn<4, false>(t.lpt))
-                              : (b_in_lds ? pieces_fn<1, true>(t.lpt) : pieces_fn<1, false>(t.lpt));
+  const void *fn = stream_fn_for(t, b_in_lds, weighted);
   if (!fn) return hipErrorInvalidValue;
-  const dim3 grid((unsigned)blocks_for(a.n_pieces, kBlock / t.lpt, max_blocks),
+  const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
+  const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, max_blocks),
                   (unsigned)t.n_slices);
-  const size_t lds = b_in_lds ? pieces_lds_bytes(a.b, a.B_rows) : 0;
-  PiecesArgs arg = a;
+  const size_t lds = b_in_lds ? stream_lds_bytes(a.b, a.B_rows) : 0;
+  StreamArgs arg = a;
   void *params[] = {&arg};
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, lds, s);
 }

@@ -93,70 +93,60 @@ void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
               keep_perm);
 }
 
-PlanHost plan_layout(const LayoutHost &L, int32_t piece_len, int32_t fan_in) {
+PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
   PlanHost P;
-  P.piece_len = piece_len;
+  P.chunk = chunk;
   P.fan_in = fan_in;
+  const int64_t n = (int64_t)L.col_a.size();
+  P.n_chunks = (n + chunk - 1) / chunk;
+  P.flush.assign(n, kNoFlush);
   struct Split {
     int32_t row;
     int64_t first, n;
   };
   std::vector<Split> splits;
-  std::vector<Piece> raw;
-  std::vector<int64_t> count_by_len(piece_len + 1, 0);
   for (int64_t q = 0; q < L.rows; ++q) {
-    const int64_t beg = L.offsets[q], deg = L.offsets[q + 1] - beg;
-    P.max_row_len = std::max(P.max_row_len, deg);
-    if (deg == 0) {
+    const int64_t beg = L.offsets[q], end = L.offsets[q + 1];
+    P.max_row_len = std::max(P.max_row_len, end - beg);
+    if (end == beg) {
       P.empty_rows.push_back((int32_t)q);
-    } else if (deg <= piece_len) {
-      raw.push_back({(int32_t)beg, (int32_t)deg, (int32_t)q, 0});
-      ++count_by_len[deg];
-    } else {
-      const int64_t np = (deg + piece_len - 1) / piece_len;
-      splits.push_back({(int32_t)q, P.n_slots, np});
-      for (int64_t k = 0; k < np; ++k) {
-        const int32_t len = (int32_t)std::min<int64_t>(piece_len, deg - k * piece_len);
-        raw.push_back({(int32_t)(beg + k * piece_len), len, (int32_t)(-(P.n_slots + k) - 1), 0});
-        ++count_by_len[len];
-      }
-      P.n_slots += np;
-      ++P.n_split_rows;
+      continue;
     }
-  }
-  // Longest pieces first (stable within a length): lane groups of one
-  // wavefront then get pieces of equal or similar length.
-  std::vector<int64_t> first(piece_len + 1, 0);
-  {
-    int64_t acc = 0;
-    for (int32_t len = piece_len; len >= 1; --len) {
-      first[len] = acc;
-      acc += count_by_len[len];
+    const int64_t c0 = beg / chunk, c1 = (end - 1) / chunk;
+    if (c0 == c1) {
+      P.flush[end - 1] = (int32_t)q;
+      continue;
     }
+    const int64_t np = c1 - c0 + 1;
+    for (int64_t k = 0; k < np; ++k) {
+      const int64_t last = std::min(end, (c0 + k + 1) * chunk) - 1;
+      P.flush[last] = (int32_t)(-(P.n_slots + k) - 1);
+    }
+    splits.push_back({(int32_t)q, P.n_slots, np});
+    P.n_slots += np;
+    ++P.n_split_rows;
   }
-  P.pieces.resize(raw.size());
-  for (const Piece &p : raw) P.pieces[first[p.len]++] = p;
-  // Combine levels: a row split into n pieces is reduced fan_in slots at a
+  // Combine levels: a row split into n partials is reduced fan_in slots at a
   // time until one task writes the row.
   for (const Split &s : splits) {
-    int64_t first_slot = s.first, n = s.n;
+    int64_t first_slot = s.first, cnt = s.n;
     size_t level = 0;
-    while (n > fan_in) {
-      const int64_t groups = (n + fan_in - 1) / fan_in;
+    while (cnt > fan_in) {
+      const int64_t groups = (cnt + fan_in - 1) / fan_in;
       const int64_t out0 = P.n_slots;
       P.n_slots += groups;
       if (P.levels.size() <= level) P.levels.resize(level + 1);
       for (int64_t g = 0; g < groups; ++g) {
-        const int64_t cnt = std::min<int64_t>(fan_in, n - g * fan_in);
-        P.levels[level].push_back({(int32_t)(first_slot + g * fan_in), (int32_t)cnt,
+        const int64_t m = std::min<int64_t>(fan_in, cnt - g * fan_in);
+        P.levels[level].push_back({(int32_t)(first_slot + g * fan_in), (int32_t)m,
                                    (int32_t)(-(out0 + g) - 1), 0});
       }
       first_slot = out0;
-      n = groups;
+      cnt = groups;
       ++level;
     }
     if (P.levels.size() <= level) P.levels.resize(level + 1);
-    P.levels[level].push_back({(int32_t)first_slot, (int32_t)n, s.row, 0});
+    P.levels[level].push_back({(int32_t)first_slot, (int32_t)cnt, s.row, 0});
   }
   return P;
 }

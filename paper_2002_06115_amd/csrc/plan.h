@@ -8,13 +8,15 @@
 //   backward dX : rows = subjects,  gathers dY[o] and R[r]
 //   backward dR : rows = relations, gathers X[s] and dY[o]
 // so the planner sorts the triples three ways (counting sorts, stable) and
-// cuts every row into pieces of at most `piece_len` triples.  A row that fits
-// in one piece is written directly by the lane group that sums it; a longer
-// row writes one double-precision partial per piece into a workspace slot and
-// the partials are added up in piece order by combine tasks, at most
+// cuts the sorted list into equal chunks, one per lane group, whatever the
+// row lengths (Zipf hubs and one-triple rows alike).  A row inside one chunk
+// is written directly by the lane group that sums it; a row that crosses chunk
+// boundaries writes one double-precision partial per chunk into a workspace
+// slot and the partials are added up in chunk order by combine tasks, at most
 // `fan_in` slots per task, over as many levels as the row needs.
 #pragma once
 
+#include <climits>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -23,11 +25,8 @@ namespace kbf {
 
 enum LayoutKind { BY_OBJ = 0, BY_SUBJ = 1, BY_REL = 2 };
 
-// One unit of work for a lane group: triples [start, start + len) of the
-// layout; dst >= 0 is the output row, dst < 0 is workspace slot -(dst + 1).
-struct Piece {
-  int32_t start, len, dst, pad;
-};
+// Marks a position whose running sum is not written out.
+constexpr int32_t kNoFlush = INT32_MIN;
 
 // Sum slots [first, first + n) in order into dst (row if >= 0, else slot -(dst + 1)).
 struct CombineTask {
@@ -43,10 +42,17 @@ struct LayoutHost {
   std::vector<int32_t> perm;      // caller index of the triple at each position
 };
 
+// The stream plan of one layout: the sorted positions are cut into chunks of
+// `chunk` consecutive positions, one chunk per lane group.  flush[p] says what
+// the lane group does after adding position p: nothing (kNoFlush), write the
+// row it just finished (>= 0), or write its partial sum of a row that crosses
+// a chunk boundary to workspace slot -(flush[p] + 1).  A row's partials are
+// numbered in chunk order and summed in that order by the combine levels.
 struct PlanHost {
-  int32_t piece_len = 0;
+  int32_t chunk = 0;
   int32_t fan_in = 0;
-  std::vector<Piece> pieces;      // longest first
+  int64_t n_chunks = 0;
+  std::vector<int32_t> flush;      // per position
   std::vector<int32_t> empty_rows;
   std::vector<std::vector<CombineTask>> levels;
   int64_t n_slots = 0;
@@ -65,7 +71,7 @@ void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                    const int32_t *subj, const int32_t *rel, const int32_t *obj,
                    const float *weight, bool keep_perm, LayoutHost out[3]);
 
-// Cuts a layout's rows into pieces and plans the combine levels.
-PlanHost plan_layout(const LayoutHost &layout, int32_t piece_len, int32_t fan_in);
+// Cuts a layout into chunks, marks the flush points and plans the combine levels.
+PlanHost plan_layout(const LayoutHost &layout, int32_t chunk, int32_t fan_in);
 
 }  // namespace kbf

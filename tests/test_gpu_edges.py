@@ -102,7 +102,7 @@ def test_empty_rows_beside_huge_rows(kbf):
     X, R, dY = rand_io(4, 32, n_e, n_r)
     kb = both(kbf, s, r, o, n_e, n_r, X, R, dY, False, "hubs+empty real")
     info = kb.info()
-    assert max(info["n_levels"]) >= 2 and info["n_empty_rows"][0] > 0
+    assert max(info["n_levels"]) >= 2 and info["n_empty_rows"][1] > 0
 
 
 def test_argument_errors(kbf):

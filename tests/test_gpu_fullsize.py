@@ -1,0 +1,86 @@
+"""Full-size parity on the large (10 M entities / 50 M triples, b = 32) and
+training-shaped (2 M entities / 20 M triples, b = 256) workloads, in the
+launch configuration bench.py times.
+
+The whole oracle is too slow here, so it computes sampled outputs one by one
+(every hub row, the largest relation, random and empty rows) and the adjoint
+identity <dY, Y> = <dX, X> = <dR, R> checks every output at once.
+"""
+import numpy as np
+import pytest
+
+import kbgen
+import oracle
+from gpu_util import assert_bitexact, assert_close, from_em
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+@pytest.fixture(scope="module")
+def kbf():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2002_06115_amd as kbf
+    return kbf
+
+
+def sample_ids(ids_deg, k_random, rng, n):
+    deg = ids_deg
+    top = np.argsort(deg)[::-1][:8]
+    zero = np.nonzero(deg == 0)[0][:4]
+    rand = rng.choice(n, size=min(k_random, n), replace=False)
+    return np.unique(np.concatenate([top, zero, rand])).astype(np.int32)
+
+
+_KB_CACHE = {}
+
+
+def run_workload(kbf, w, integer):
+    import torch
+    print(f"[fullsize] generating {w.label} integer={integer}", flush=True)
+    if w.name not in _KB_CACHE:
+        _KB_CACHE.clear()
+        _KB_CACHE[w.name] = kbgen.make_kb(w)
+    kb = _KB_CACHE[w.name]
+    if integer:
+        X, R, dY = kbgen.make_integer_inputs(w)
+    else:
+        X, R, dY = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
+    print(f"[fullsize] kb_create {w.label}", flush=True)
+    gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
+    em = lambda a: torch.from_numpy(a).cuda().t().contiguous()
+    Xe, Re, dYe = em(X), em(R), em(dY)
+    Y = gkb.follow(Xe, Re)
+    dX, dR = gkb.follow_backward(Xe, Re, dYe)
+    torch.cuda.synchronize()
+    print(f"[fullsize] GPU pass done {w.label}", flush=True)
+    rng = np.random.default_rng(7)
+    objs = sample_ids(np.bincount(kb.obj, minlength=w.n_entities), 48, rng, w.n_entities)
+    subs = sample_ids(np.bincount(kb.subj, minlength=w.n_entities), 48, rng, w.n_entities)
+    rels = sample_ids(np.bincount(kb.rel, minlength=w.n_relations), 8, rng, w.n_relations)
+    args = (kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
+    want_y = oracle.sampled(oracle.SAMPLE_Y, *args, objs, X=X, R=R)
+    want_dx = oracle.sampled(oracle.SAMPLE_DX, *args, subs, R=R, dY=dY)
+    want_dr = oracle.sampled(oracle.SAMPLE_DR, *args, rels, X=X, dY=dY)
+    idx = lambda t, ids: t[torch.from_numpy(ids.astype(np.int64)).cuda()].t().contiguous().cpu().numpy()
+    got = (idx(Y, objs), idx(dX, subs), idx(dR, rels))
+    check = assert_bitexact if integer else assert_close
+    for name, g, e in zip(("Y", "dX", "dR"), got, (want_y, want_dx, want_dr)):
+        check(g, e, f"{w.name} {name} sampled")
+    # Adjoint identity over every output (float64 sums of the float32 results).
+    d = lambda a, b: float((a.double() * b.double()).sum())
+    yy, xx, rr = d(dYe, Y), d(dX, Xe), d(dR, Re)
+    scale = float((dYe.double().abs() * Y.double().abs()).sum()) + 1e-30
+    assert abs(yy - xx) <= 1e-6 * scale and abs(yy - rr) <= 1e-6 * scale, (yy, xx, rr)
+    gkb.close()
+
+
+@pytest.mark.parametrize("integer", [True, False])
+def test_large_fullsize(kbf, integer):
+    run_workload(kbf, kbgen.LARGE, integer)
+
+
+@pytest.mark.parametrize("integer", [True, False])
+def test_train_fullsize(kbf, integer):
+    run_workload(kbf, kbgen.TRAIN, integer)

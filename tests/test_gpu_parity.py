@@ -4,7 +4,7 @@ Integer-valued inputs (k-hot X, one-hot R, dY = 1) must match bit for bit;
 real-valued inputs within |gpu - oracle| <= 1e-7 + 1e-5 |oracle| elementwise.
 Sizes: the tiny and MetaQA-shaped workloads at full size, the large and
 training-shaped workloads scaled down so the whole oracle runs in seconds
-(still thousands of pieces, split hub rows and ragged tails); the full-size
+(still thousands of chunks, split hub rows and ragged tails); the full-size
 large and training workloads are in test_gpu_fullsize.py.
 """
 import numpy as np
