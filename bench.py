@@ -27,8 +27,8 @@ sys.path.insert(0, ROOT)
 METRIC = "triple·batch products/sec for kb_follow fwd+bwd; achieved HBM GB/s vs peak"
 PEAK_HBM_GBPS = 8000.0
 DOMINANT_KERNEL_NAMES = {
-    "fwd_stream": "stream_kernel (forward: objects, gathers X)",
-    "dx_stream": "stream_kernel (dX: subjects, gathers dY)",
+    "fwd_stream": "stream_kernel (forward: objects, gathers X and R)",
+    "dx_stream": "stream_kernel (dX: subjects, gathers dY and R)",
     "dr_stream": "stream_kernel (dR: relations, gathers X and dY)",
 }
 
@@ -54,6 +54,25 @@ def pass_bytes(kb, b, phase):
         comp = idx + 4 * (n_r + 1) + 4 * b * (len(np.unique(kb.subj)) + len(np.unique(kb.obj))) \
             + 4 * b * n_r
     return float(gather), float(comp)
+
+
+def measured_traffic(workload, b, phase):
+    """DRAM bytes of one launch from the committed rocprofv3 counters, if they
+    were taken on the device code that is built now (same fingerprint)."""
+    import glob
+    fp_path = os.path.join(ROOT, "paper_2002_06115_amd", "_lib", "kernels.fingerprint")
+    if not os.path.exists(fp_path):
+        return None
+    fp = open(fp_path).read().strip()
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*.json")):
+        try:
+            prof = json.load(open(path))
+        except (OSError, ValueError):
+            continue
+        if prof.get("workload") == workload and prof.get("batch") == b \
+                and prof.get("fingerprint") == fp and phase in prof.get("per_launch", {}):
+            return float(prof["per_launch"][phase]["bytes"])
+    return None
 
 
 def cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads):
@@ -166,15 +185,20 @@ def main():
         dom = max(("fwd_stream", "dx_stream", "dr_stream"), key=lambda p: phases[p][0])
         ms_avg = phases[dom][0] / max(1, phases[dom][1])
         gather_b, comp_b = pass_bytes(kb, b, dom)
-        achieved = gather_b / (ms_avg * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+        sec = ms_avg * 1e-3
+        traffic = measured_traffic(w.name, b, dom)
+        roof = {"bound": "hbm", "achieved": round(comp_b / sec / 1e9, 1), "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s", "frac": round(comp_b / sec / 1e9 / PEAK_HBM_GBPS, 4),
+                "traffic": traffic,
                 "kernel": DOMINANT_KERNEL_NAMES[dom], "kernel_ms": round(ms_avg, 4),
-                "bytes_model": "gather: 8 B of ids per triple + every triple's gathered "
-                               "b-wide rows + output rows",
-                "algorithmic_bytes": gather_b,
-                "compulsory_bytes": comp_b,
-                "compulsory_GBps": round(comp_b / (ms_avg * 1e-3) / 1e9, 1)}
+                "bytes_model": "compulsory: 8 B of ids per triple, row offsets, every distinct "
+                               "gathered row once, R, every output row once",
+                "algorithmic_bytes": comp_b,
+                "gather_model_bytes": gather_b,
+                "gather_model_GBps": round(gather_b / sec / 1e9, 1)}
+        if traffic:
+            roof["hbm_measured_GBps"] = round(traffic / sec / 1e9, 1)
+            roof["hbm_measured_frac"] = round(traffic / sec / 1e9 / PEAK_HBM_GBPS, 4)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -23,7 +23,7 @@ import os
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "_lib", "libkbfollow.so")
+LIB_PATH = os.environ.get("KBFOLLOW_LIB") or os.path.join(_PKG, "_lib", "libkbfollow.so")
 
 KB_OK, KB_EINVAL, KB_ERANGE, KB_ENOMEM, KB_EHIP, KB_ENOTSUP = range(6)
 PHASES = ("fwd_stream", "fwd_combine", "fwd_zero", "dx_stream", "dx_combine", "dx_zero",

@@ -35,29 +35,54 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libkbfollow)")
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(OUT_DIR, exist_ok=True)
-    os.makedirs(BUILD_DIR, exist_ok=True)
+def build(verbose: bool = False, defines=(), out=None, build_dir=None) -> str:
+    """Compile and link the library; ``defines`` are extra -D flags (tuning
+    experiments), ``out``/``build_dir`` redirect the outputs."""
+    out = out or LIB
+    bdir = build_dir or BUILD_DIR
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    os.makedirs(bdir, exist_ok=True)
+    extra = [f"-D{d}" for d in defines]
     cc = hipcc()
     objs = []
     for src in SOURCES:
         path = os.path.join(CSRC, src)
-        obj = os.path.join(BUILD_DIR, src + ".o")
+        obj = os.path.join(bdir, src + ".o")
         if src.endswith(".hip"):
-            cmd = [cc, "-x", "hip", *DEVICE_FLAGS, *COMMON_FLAGS, "-c", path, "-o", obj]
+            cmd = [cc, "-x", "hip", *DEVICE_FLAGS, *COMMON_FLAGS, *extra, "-c", path, "-o", obj]
         else:
             cmd = [cc, *COMMON_FLAGS, "-c", path, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.check_call(cmd)
         objs.append(obj)
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     cmd = [cc, *DEVICE_FLAGS, "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    fingerprint(defines, os.path.join(os.path.dirname(out), "kernels.fingerprint"), bdir)
+    return out
+
+
+def fingerprint(defines, path, bdir) -> str:
+    """sha256 of the gfx950 assembly of kernels.hip (compiler-unique ids
+    removed): identifies the device code that rocprofv3 counters were taken on."""
+    import hashlib
+    asm = os.path.join(bdir, "kernels.s")
+    cmd = [hipcc(), "-x", "hip", "--cuda-device-only", "-S", *DEVICE_FLAGS, *COMMON_FLAGS,
+           *[f"-D{d}" for d in defines], os.path.join(CSRC, "kernels.hip"), "-o", asm]
+    subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
+    h = hashlib.sha256()
+    with open(asm) as f:
+        for line in f:
+            if "__hip_cuid" not in line and not line.lstrip().startswith((".file", ".ident")):
+                h.update(line.encode())
+    digest = h.hexdigest()
+    with open(path, "w") as f:
+        f.write(digest + "\n")
+    return digest
 
 
 if __name__ == "__main__":

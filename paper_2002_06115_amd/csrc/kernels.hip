@@ -36,8 +36,32 @@ namespace kbf {
 
 namespace {
 
-constexpr int kBlock = 256;   // threads per workgroup (4 wavefronts of 64)
-constexpr int kUnroll = 8;    // triples whose loads a lane group keeps in flight
+#ifndef KBF_UNROLL
+#define KBF_UNROLL 8
+#endif
+#ifndef KBF_NT_ENTRIES
+#define KBF_NT_ENTRIES 0
+#endif
+#ifndef KBF_NT_STORES
+#define KBF_NT_STORES 0
+#endif
+
+constexpr int kBlock = 256;         // threads per workgroup (4 wavefronts of 64)
+constexpr int kUnroll = KBF_UNROLL; // triples whose loads a lane group keeps in flight
+
+// The triple stream is read once per pass: non-temporal loads keep it from
+// evicting the gathered activation rows that Zipf-hot ids reuse from cache.
+typedef int native_int4 __attribute__((ext_vector_type(4)));
+typedef float native_float4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ int4 load_entry(const int4 *p) {
+#if KBF_NT_ENTRIES
+  const native_int4 v = __builtin_nontemporal_load(reinterpret_cast<const native_int4 *>(p));
+  return make_int4(v.x, v.y, v.z, v.w);
+#else
+  return *p;
+#endif
+}
 
 template <int VEC>
 __device__ __forceinline__ void load_row(const float *__restrict__ p, float (&v)[VEC]) {
@@ -55,8 +79,13 @@ __device__ __forceinline__ void load_row(const float *__restrict__ p, float (&v)
 template <int VEC>
 __device__ __forceinline__ void store_row(float *__restrict__ p, const double (&acc)[VEC]) {
   if constexpr (VEC == 4) {
+#if KBF_NT_STORES
+    native_float4 v = {(float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]};
+    __builtin_nontemporal_store(v, reinterpret_cast<native_float4 *>(p));
+#else
     *reinterpret_cast<float4 *>(p) =
         make_float4((float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]);
+#endif
   } else {
     *p = (float)acc[0];
   }
@@ -130,7 +159,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
     // step's gathers are in flight.
     int4 e_next[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) e_next[u] = a.entries[min(p0 + u, p1 - 1)];
+    for (int u = 0; u < kUnroll; ++u) e_next[u] = load_entry(a.entries + min(p0 + u, p1 - 1));
     for (int64_t p = p0; p < p1; p += kUnroll) {
       const int cnt = (int)min((int64_t)kUnroll, p1 - p);
       int4 e[kUnroll];
@@ -146,7 +175,8 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
           load_row<VEC>(a.B + (size_t)e[u].y * bb + cl, xb[u]);
       }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) e_next[u] = a.entries[min(p + kUnroll + u, p1 - 1)];
+      for (int u = 0; u < kUnroll; ++u)
+        e_next[u] = load_entry(a.entries + min(p + kUnroll + u, p1 - 1));
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         if (u < cnt) {
