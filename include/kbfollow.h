@@ -78,7 +78,7 @@ typedef enum {
  * The three sorted layouts (by object, by subject, by relation) and their
  * work plans are built on the host and uploaded; the host copies are freed.
  * Device memory held: 16 bytes per triple per layout (48 per triple) plus
- * small plans.
+ * small plans.  Building takes seven stable counting passes over the triples.
  * Errors: KB_EINVAL (sizes, null pointers), KB_ERANGE (an id out of range;
  * checked before any device work), KB_ENOMEM, KB_EHIP.
  */
@@ -160,9 +160,11 @@ kb_status kb_get_info(const kb_t *kb, kb_info_t *info);
 
 /*
  * The sorted layout kb_create builds, computed on the host only (no GPU needed).
- *   which = 0: by object  (rows = objects,   key order (o, s, r)), col_a = subj, col_b = rel
- *   which = 1: by subject (rows = subjects,  key order (s, o, r)), col_a = obj,  col_b = rel
- *   which = 2: by relation(rows = relations, key order (r, s, o)), col_a = subj, col_b = obj
+ *   which = 0: by object   (rows = objects,   key order (o, r, s)), col_a = subj, col_b = rel
+ *   which = 1: by subject  (rows = subjects,  key order (s, r, o)), col_a = obj,  col_b = rel
+ *   which = 2: by relation (rows = relations, key order (r, s, o)), col_a = obj,  col_b = subj
+ *   (col_a is the id gathered for every triple, col_b the id read once per run
+ *   of equal col_b inside a row)
  *   offsets : HOST int32 [rows + 1]; row q's triples are positions offsets[q] .. offsets[q+1]-1
  *   col_a, col_b, perm : HOST int32 [N_T]; perm[p] = caller index of the triple at position p
  * Any output pointer may be NULL.  Same validation and errors as kb_create.

@@ -25,7 +25,7 @@ SOURCES = ["kernels.hip", "api.cpp", "plan.cpp"]
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
                 "-packed-fp32-ops"]
 COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-command-line-argument",
-                "-I", INCLUDE, "-I", CSRC]
+                "-I", INCLUDE]
 
 
 def hipcc() -> str:
@@ -35,9 +35,10 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libkbfollow)")
 
 
-def build(verbose: bool = False, defines=(), out=None, build_dir=None) -> str:
+def build(verbose: bool = False, defines=(), out=None, build_dir=None, src_dir=None) -> str:
     """Compile and link the library; ``defines`` are extra -D flags (tuning
-    experiments), ``out``/``build_dir`` redirect the outputs."""
+    experiments), ``out``/``build_dir``/``src_dir`` redirect inputs and outputs."""
+    csrc = src_dir or CSRC
     out = out or LIB
     bdir = build_dir or BUILD_DIR
     os.makedirs(os.path.dirname(out), exist_ok=True)
@@ -46,12 +47,13 @@ def build(verbose: bool = False, defines=(), out=None, build_dir=None) -> str:
     cc = hipcc()
     objs = []
     for src in SOURCES:
-        path = os.path.join(CSRC, src)
+        path = os.path.join(csrc, src)
         obj = os.path.join(bdir, src + ".o")
         if src.endswith(".hip"):
-            cmd = [cc, "-x", "hip", *DEVICE_FLAGS, *COMMON_FLAGS, *extra, "-c", path, "-o", obj]
+            cmd = [cc, "-x", "hip", *DEVICE_FLAGS, *COMMON_FLAGS, "-I", csrc, *extra, "-c", path,
+                   "-o", obj]
         else:
-            cmd = [cc, *COMMON_FLAGS, "-c", path, "-o", obj]
+            cmd = [cc, *COMMON_FLAGS, "-I", csrc, "-c", path, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.check_call(cmd)
@@ -62,17 +64,17 @@ def build(verbose: bool = False, defines=(), out=None, build_dir=None) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(tmp, out)
-    fingerprint(defines, os.path.join(os.path.dirname(out), "kernels.fingerprint"), bdir)
+    fingerprint(defines, os.path.join(os.path.dirname(out), "kernels.fingerprint"), bdir, csrc)
     return out
 
 
-def fingerprint(defines, path, bdir) -> str:
+def fingerprint(defines, path, bdir, csrc=CSRC) -> str:
     """sha256 of the gfx950 assembly of kernels.hip (compiler-unique ids
     removed): identifies the device code that rocprofv3 counters were taken on."""
     import hashlib
     asm = os.path.join(bdir, "kernels.s")
     cmd = [hipcc(), "-x", "hip", "--cuda-device-only", "-S", *DEVICE_FLAGS, *COMMON_FLAGS,
-           *[f"-D{d}" for d in defines], os.path.join(CSRC, "kernels.hip"), "-o", asm]
+           "-I", csrc, *[f"-D{d}" for d in defines], os.path.join(csrc, "kernels.hip"), "-o", asm]
     subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
     h = hashlib.sha256()
     with open(asm) as f:

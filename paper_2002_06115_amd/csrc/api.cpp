@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
 #include <cstdlib>
 #include <cstring>
 #include <new>
@@ -124,9 +125,11 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
     float w = wt ? H.weight[p] : 1.0f;
     int32_t wbits;
     std::memcpy(&wbits, &w, sizeof wbits);
-    entries[p] = make_int4(H.col_a[p], H.col_b[p], P.flush[p], wbits);
+    const int32_t a = H.col_a[p] | (P.run_end[p] ? INT32_MIN : 0);  // top bit: run ends here
+    entries[p] = make_int4(a, H.col_b[p], P.flush[p], wbits);
   }
   std::vector<int32_t>().swap(P.flush);
+  std::vector<uint8_t>().swap(P.run_end);
   std::vector<int4> ctasks;
   D.level_begin.assign(1, 0);
   for (const auto &lv : P.levels) {
@@ -448,7 +451,8 @@ kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const fl
       if (st != KB_OK) return st;
     }
     if (want_dr) {
-      st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_STREAM, X, dY, kb->n_entities, false, b, dR,
+      // By relation, runs of equal subject: dR[k] = sum over runs of X[s] (.) sum of dY[o].
+      st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_STREAM, dY, X, kb->n_entities, false, b, dR,
                     workspace, s);
       if (st != KB_OK) return st;
     }

@@ -31,6 +31,7 @@
 #include "kernels.h"
 
 #include <climits>
+#include <utility>
 
 namespace kbf {
 
@@ -39,28 +40,38 @@ namespace {
 #ifndef KBF_UNROLL
 #define KBF_UNROLL 8
 #endif
-#ifndef KBF_NT_ENTRIES
-#define KBF_NT_ENTRIES 0
-#endif
-#ifndef KBF_NT_STORES
-#define KBF_NT_STORES 0
-#endif
 
 constexpr int kBlock = 256;         // threads per workgroup (4 wavefronts of 64)
 constexpr int kUnroll = KBF_UNROLL; // triples whose loads a lane group keeps in flight
 
-// The triple stream is read once per pass: non-temporal loads keep it from
-// evicting the gathered activation rows that Zipf-hot ids reuse from cache.
-typedef int native_int4 __attribute__((ext_vector_type(4)));
-typedef float native_float4 __attribute__((ext_vector_type(4)));
+// Buffer-resource word 3 for gfx9-family raw buffers, and an offset past any
+// buffer this library makes: such a load returns zeros without touching memory.
+constexpr int kRawBufferWord3 = 0x00020000;
+constexpr uint32_t kOutOfRange = 0xFFFFFFF0u;
 
-__device__ __forceinline__ int4 load_entry(const int4 *p) {
-#if KBF_NT_ENTRIES
-  const native_int4 v = __builtin_nontemporal_load(reinterpret_cast<const native_int4 *>(p));
-  return make_int4(v.x, v.y, v.z, v.w);
-#else
-  return *p;
-#endif
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F &f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time.
+template <int N, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Value of lane SRC of this lane's group of LPT lanes (LPT a power of two).
+// Groups of up to 32 lanes use ds_swizzle's bitmask mode (no LDS memory is
+// touched): source lane = (lane & and_mask) | SRC within each 32-lane half.
+template <int LPT, int SRC>
+__device__ __forceinline__ int group_bcast(int v) {
+  if constexpr (LPT == 1) {
+    return v;
+  } else if constexpr (LPT == 64) {
+    return __builtin_amdgcn_readlane(v, SRC);
+  } else {
+    constexpr int and_mask = 0x1f & ~(LPT - 1);
+    return __builtin_amdgcn_ds_swizzle(v, and_mask | (SRC << 5));
+  }
 }
 
 template <int VEC>
@@ -76,16 +87,26 @@ __device__ __forceinline__ void load_row(const float *__restrict__ p, float (&v)
   }
 }
 
+// VEC floats at byte offset `off` of a raw buffer (zeros when off is past its end).
+template <int VEC>
+__device__ __forceinline__ void load_row_buffer(__amdgpu_buffer_rsrc_t rsrc, uint32_t off,
+                                                float (&v)[VEC]) {
+  if constexpr (VEC == 4) {
+    const auto t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)off, 0, 0);
+    v[0] = __int_as_float(t[0]);
+    v[1] = __int_as_float(t[1]);
+    v[2] = __int_as_float(t[2]);
+    v[3] = __int_as_float(t[3]);
+  } else {
+    v[0] = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)off, 0, 0));
+  }
+}
+
 template <int VEC>
 __device__ __forceinline__ void store_row(float *__restrict__ p, const double (&acc)[VEC]) {
   if constexpr (VEC == 4) {
-#if KBF_NT_STORES
-    native_float4 v = {(float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]};
-    __builtin_nontemporal_store(v, reinterpret_cast<native_float4 *>(p));
-#else
     *reinterpret_cast<float4 *>(p) =
         make_float4((float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]);
-#endif
   } else {
     *p = (float)acc[0];
   }
@@ -118,9 +139,22 @@ __device__ __forceinline__ void store_slot(double *__restrict__ p, const double 
 // One lane group (LPT lanes) per chunk of the sorted triple stream; chunks
 // are visited grid-stride so a capped (persistent) grid works too.  Every
 // chunk holds the same number of positions, so the work is balanced whatever
-// the row lengths.  With B_IN_LDS the workgroup first copies B's column slice
-// [B_rows][W] into LDS (the relation table R is tiny: N_R x b floats).
-template <int VEC, int LPT, bool B_IN_LDS, bool WEIGHTED>
+// the row lengths.
+//
+// Inside a row the positions come in runs of equal B id.  The group sums the
+// A rows of a run (in double) and multiplies the sum by the B row once, at the
+// run's last position (entry.x has its top bit set there): B is read once per
+// run, not once per triple.  Where B comes from:
+//   kBBuffer : a raw buffer load per lane whose offset is out of range except
+//              at run ends, so the load never sits behind a branch and the
+//              lanes that need no B row generate no memory traffic;
+//   kBLds    : the workgroup first copies B's column slice into LDS (small
+//              tables only), lane-chunk j of row k kept at j ^ (k mod LPT) so
+//              the random rows of one wavefront spread over the banks;
+//   kBGlobal : a plain load of every position's B row (B of 4 GB or more).
+enum BSource { kBGlobal = 0, kBBuffer = 1, kBLds = 2 };
+
+template <int VEC, int LPT, int BSRC, bool WEIGHTED>
 __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
@@ -132,15 +166,23 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   const bool active = c < a.b;
   const size_t bb = (size_t)a.b;
 
-  if constexpr (B_IN_LDS) {
+  auto lds_chunk = [](int64_t k, int j) -> int64_t {
+    return k * W + (int64_t)((j ^ (int)(k & (LPT - 1))) * VEC);
+  };
+  if constexpr (BSRC == kBLds) {
     const int64_t total = a.B_rows * W;
     for (int64_t e = threadIdx.x; e < total; e += kBlock) {
       const int64_t k = e / W;
-      const int cc = col0 + (int)(e - k * W);
-      lds_b[e] = cc < a.b ? a.B[k * bb + cc] : 0.0f;
+      const int col = (int)(e - k * W);
+      const int cc = col0 + col;
+      lds_b[lds_chunk(k, col / VEC) + col % VEC] = cc < a.b ? a.B[k * bb + cc] : 0.0f;
     }
     __syncthreads();
   }
+  // (Only used with kBBuffer, where B is known to be under 4 GB.)
+  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float *>(a.B), 0, (int)(uint32_t)(a.B_rows * a.b * sizeof(float)),
+      kRawBufferWord3);
 
   // Loads never sit behind a branch, so all kUnroll gathers of a step are in
   // flight together: lanes past b read column 0 and store nothing, and the
@@ -148,45 +190,72 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   const int cl = active ? c : 0;
   const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
   const int64_t stride = (int64_t)gridDim.x * GPB;
+
+  // Each lane loads K of a step's kUnroll entries (lane + k * LPT) and the
+  // group shares them by broadcast, so one load instruction fetches the
+  // entries of every lane group in the wavefront.
+  constexpr int K = (kUnroll + LPT - 1) / LPT;
+  auto fetch = [&](int64_t p, int64_t p1, int4 (&mine)[K]) {
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+      mine[k] = a.entries[min(p + min(lane + k * LPT, kUnroll - 1), p1 - 1)];
+  };
+
   for (int64_t g = (int64_t)blockIdx.x * GPB + grp; g < n_chunks; g += stride) {
     const int64_t p0 = g * a.chunk;
     const int64_t p1 = min(p0 + (int64_t)a.chunk, a.n);
-    double acc[VEC];
+    double acc[VEC], run[VEC];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) acc[v] = 0.0;
+    for (int v = 0; v < VEC; ++v) acc[v] = run[v] = 0.0;
 
     // Software pipeline: the entries of the next step are loaded while this
     // step's gathers are in flight.
-    int4 e_next[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) e_next[u] = load_entry(a.entries + min(p0 + u, p1 - 1));
+    int4 mine_next[K];
+    fetch(p0, p1, mine_next);
     for (int64_t p = p0; p < p1; p += kUnroll) {
       const int cnt = (int)min((int64_t)kUnroll, p1 - p);
       int4 e[kUnroll];
       float xa[kUnroll][VEC], xb[kUnroll][VEC];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) e[u] = e_next[u];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        load_row<VEC>(a.A + (size_t)e[u].x * bb + cl, xa[u]);
-        if constexpr (B_IN_LDS)
-          load_row<VEC>(lds_b + (size_t)e[u].y * W + lane * VEC, xb[u]);
-        else
-          load_row<VEC>(a.B + (size_t)e[u].y * bb + cl, xb[u]);
-      }
+      static_for<kUnroll>([&](auto uc) {
+        constexpr int u = decltype(uc)::value;
+        const int4 m = mine_next[u / LPT];
+        e[u] = make_int4(group_bcast<LPT, u % LPT>(m.x), group_bcast<LPT, u % LPT>(m.y),
+                         group_bcast<LPT, u % LPT>(m.z),
+                         WEIGHTED ? group_bcast<LPT, u % LPT>(m.w) : 0);
+      });
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
-        e_next[u] = load_entry(a.entries + min(p + kUnroll + u, p1 - 1));
+        load_row<VEC>(a.A + (size_t)(e[u].x & 0x7fffffff) * bb + cl, xa[u]);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        if constexpr (BSRC == kBBuffer) {
+          const uint32_t off =
+              e[u].x < 0 ? (uint32_t)(((size_t)e[u].y * bb + cl) * sizeof(float)) : kOutOfRange;
+          load_row_buffer<VEC>(brsrc, off, xb[u]);
+        } else if constexpr (BSRC == kBLds) {
+          load_row<VEC>(lds_b + lds_chunk(e[u].y, lane), xb[u]);
+        } else {
+          load_row<VEC>(a.B + (size_t)e[u].y * bb + cl, xb[u]);
+        }
+      }
+      fetch(p + kUnroll, p1, mine_next);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         if (u < cnt) {
           if constexpr (WEIGHTED) {
             const double w = (double)__int_as_float(e[u].w);
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[v] += w * (double)xa[u][v] * (double)xb[u][v];
+            for (int v = 0; v < VEC; ++v) run[v] += w * (double)xa[u][v];
           } else {
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[v] += (double)xa[u][v] * (double)xb[u][v];
+            for (int v = 0; v < VEC; ++v) run[v] += (double)xa[u][v];
+          }
+          if (e[u].x < 0) {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+              acc[v] += run[v] * (double)xb[u][v];
+              run[v] = 0.0;
+            }
           }
           const int f = e[u].z;
           if (f != INT_MIN) {
@@ -263,27 +332,32 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__rest
   }
 }
 
-template <int VEC, bool LDS, bool WT>
+template <int VEC, int BSRC, bool WT>
 const void *stream_fn(int lpt) {
   switch (lpt) {
-    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, LDS, WT>);
-    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, LDS, WT>);
-    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, LDS, WT>);
-    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, LDS, WT>);
-    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, LDS, WT>);
-    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, LDS, WT>);
-    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, LDS, WT>);
+    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, BSRC, WT>);
+    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, BSRC, WT>);
+    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, BSRC, WT>);
+    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, BSRC, WT>);
+    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, BSRC, WT>);
+    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, BSRC, WT>);
+    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, BSRC, WT>);
   }
   return nullptr;
 }
 
-const void *stream_fn_for(const ColumnTiling &t, bool lds, bool wt) {
-  if (t.vec == 4) {
-    if (lds) return wt ? stream_fn<4, true, true>(t.lpt) : stream_fn<4, true, false>(t.lpt);
-    return wt ? stream_fn<4, false, true>(t.lpt) : stream_fn<4, false, false>(t.lpt);
+template <int VEC>
+const void *stream_fn_vec(int lpt, int bsrc, bool wt) {
+  switch (bsrc) {
+    case kBGlobal: return wt ? stream_fn<VEC, kBGlobal, true>(lpt) : stream_fn<VEC, kBGlobal, false>(lpt);
+    case kBBuffer: return wt ? stream_fn<VEC, kBBuffer, true>(lpt) : stream_fn<VEC, kBBuffer, false>(lpt);
+    case kBLds: return wt ? stream_fn<VEC, kBLds, true>(lpt) : stream_fn<VEC, kBLds, false>(lpt);
   }
-  if (lds) return wt ? stream_fn<1, true, true>(t.lpt) : stream_fn<1, true, false>(t.lpt);
-  return wt ? stream_fn<1, false, true>(t.lpt) : stream_fn<1, false, false>(t.lpt);
+  return nullptr;
+}
+
+const void *stream_fn_for(const ColumnTiling &t, int bsrc, bool wt) {
+  return t.vec == 4 ? stream_fn_vec<4>(t.lpt, bsrc, wt) : stream_fn_vec<1>(t.lpt, bsrc, wt);
 }
 
 template <int VEC>
@@ -329,7 +403,7 @@ size_t stream_lds_bytes(int32_t b, int64_t B_rows) {
 hipError_t prepare_stream_lds(int32_t b, size_t bytes) {
   const ColumnTiling t = column_tiling(b);
   for (bool wt : {false, true}) {
-    const void *fn = stream_fn_for(t, true, wt);
+    const void *fn = stream_fn_for(t, kBLds, wt);
     if (!fn) return hipErrorInvalidValue;
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess) return e;
@@ -341,7 +415,10 @@ hipError_t launch_stream(const StreamArgs &a, bool weighted, bool b_in_lds, int 
                          hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(a.b);
-  const void *fn = stream_fn_for(t, b_in_lds, weighted);
+  // Raw-buffer offsets are 32-bit: B of 4 GB or more takes plain loads.
+  const bool fits = (uint64_t)a.B_rows * (uint64_t)a.b * sizeof(float) <= (uint64_t)kOutOfRange;
+  const int bsrc = b_in_lds ? kBLds : (fits ? kBBuffer : kBGlobal);
+  const void *fn = stream_fn_for(t, bsrc, weighted);
   if (!fn) return hipErrorInvalidValue;
   const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
   const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, max_blocks),

@@ -3,9 +3,10 @@
 // The reified KB of Sec. 2.3 keeps, per triple, its subject, object and
 // relation ids (the one nonzero of row l in M_subj, M_obj and M_rel).  Here
 // the triples are sorted three ways with stable counting sorts (O(N_T + N)
-// each): by (s, o, r), by (o, s, r) and by (r, s, o).  The secondary keys put
-// equal gathered ids next to each other inside a row, so repeated rows of X or
-// dY are read back to back.
+// each): by (o, r, s), by (s, r, o) and by (r, s, o).  The secondary key
+// groups each row into runs of equal second operand (the relation for the
+// forward and dX passes, the subject for dR), so the kernels read that
+// operand once per run instead of once per triple.
 #include "plan.h"
 
 #include <algorithm>
@@ -75,21 +76,26 @@ void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
   std::vector<int32_t> ident(n_triples), t1, t2, by_subj, by_obj, by_rel;
   for (int64_t l = 0; l < n_triples; ++l) ident[l] = (int32_t)l;
   std::vector<int32_t> off_subj, off_obj, off_rel;
-  // (s, o, r): least significant key first.
-  counting_sort(rel, n_relations, ident, t1, nullptr);
-  counting_sort(obj, n_entities, t1, t2, nullptr);
+  // Least significant key first; every pass is stable.
+  // (s, r, o): by subject, relation runs inside a row, objects ascending.
+  counting_sort(obj, n_entities, ident, t1, nullptr);
+  counting_sort(rel, n_relations, t1, t2, nullptr);
   counting_sort(subj, n_entities, t2, by_subj, &off_subj);
+  // (r, s, o): the (s, r, o) order re-sorted by relation.
+  counting_sort(rel, n_relations, by_subj, by_rel, &off_rel);
+  // (o, r, s): by object, relation runs inside a row, subjects ascending.
+  counting_sort(subj, n_entities, ident, t1, nullptr);
+  counting_sort(rel, n_relations, t1, t2, nullptr);
+  counting_sort(obj, n_entities, t2, by_obj, &off_obj);
   std::vector<int32_t>().swap(ident);
   std::vector<int32_t>().swap(t1);
   std::vector<int32_t>().swap(t2);
-  // (o, s, r) and (r, s, o) from the (s, o, r) order.
-  counting_sort(obj, n_entities, by_subj, by_obj, &off_obj);
-  counting_sort(rel, n_relations, by_subj, by_rel, &off_rel);
+  // col_a is gathered for every triple, col_b once per run of equal col_b.
   fill_layout(out[BY_OBJ], n_entities, std::move(by_obj), std::move(off_obj), subj, rel, weight,
               keep_perm);
   fill_layout(out[BY_SUBJ], n_entities, std::move(by_subj), std::move(off_subj), obj, rel,
               weight, keep_perm);
-  fill_layout(out[BY_REL], n_relations, std::move(by_rel), std::move(off_rel), subj, obj, weight,
+  fill_layout(out[BY_REL], n_relations, std::move(by_rel), std::move(off_rel), obj, subj, weight,
               keep_perm);
 }
 
@@ -100,6 +106,7 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
   const int64_t n = (int64_t)L.col_a.size();
   P.n_chunks = (n + chunk - 1) / chunk;
   P.flush.assign(n, kNoFlush);
+  P.run_end.assign(n, 0);
   struct Split {
     int32_t row;
     int64_t first, n;
@@ -112,6 +119,8 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
       P.empty_rows.push_back((int32_t)q);
       continue;
     }
+    for (int64_t p = beg; p < end; ++p)
+      P.run_end[p] = (p + 1 == end || (p + 1) % chunk == 0 || L.col_b[p + 1] != L.col_b[p]);
     const int64_t c0 = beg / chunk, c1 = (end - 1) / chunk;
     if (c0 == c1) {
       P.flush[end - 1] = (int32_t)q;

@@ -4,9 +4,9 @@
 // M_subj, M_obj and M_rel map triple l to its subject, object and relation.
 // Each of the library's three passes is a segmented sum over the triples
 // grouped by one of those ids:
-//   forward  Y  : rows = objects,   gathers X[s] and R[r]   (Eq. 4)
-//   backward dX : rows = subjects,  gathers dY[o] and R[r]
-//   backward dR : rows = relations, gathers X[s] and dY[o]
+//   forward  Y  : rows = objects,   sum over r-runs of R[r] (.) sum X[s]   (Eq. 4)
+//   backward dX : rows = subjects,  sum over r-runs of R[r] (.) sum dY[o]
+//   backward dR : rows = relations, sum over s-runs of X[s] (.) sum dY[o]
 // so the planner sorts the triples three ways (counting sorts, stable) and
 // cuts the sorted list into equal chunks, one per lane group, whatever the
 // row lengths (Zipf hubs and one-triple rows alike).  A row inside one chunk
@@ -36,8 +36,8 @@ struct CombineTask {
 struct LayoutHost {
   int64_t rows = 0;
   std::vector<int32_t> offsets;   // rows + 1
-  std::vector<int32_t> col_a;     // gathered id of the first operand, per position
-  std::vector<int32_t> col_b;     // id of the second operand, per position
+  std::vector<int32_t> col_a;     // id of the operand gathered for every triple (A)
+  std::vector<int32_t> col_b;     // id of the operand read once per run (B)
   std::vector<float> weight;      // per position, empty for a hard KB
   std::vector<int32_t> perm;      // caller index of the triple at each position
 };
@@ -48,11 +48,15 @@ struct LayoutHost {
 // row it just finished (>= 0), or write its partial sum of a row that crosses
 // a chunk boundary to workspace slot -(flush[p] + 1).  A row's partials are
 // numbered in chunk order and summed in that order by the combine levels.
+// Inside a row the positions form runs of equal col_b; run_end[p] marks the
+// last position of a run (a row end or chunk end also ends a run), where the
+// kernel multiplies the run's sum of A rows by the B row once.
 struct PlanHost {
   int32_t chunk = 0;
   int32_t fan_in = 0;
   int64_t n_chunks = 0;
   std::vector<int32_t> flush;      // per position
+  std::vector<uint8_t> run_end;    // per position: last of a run of equal col_b (or of a chunk)
   std::vector<int32_t> empty_rows;
   std::vector<std::vector<CombineTask>> levels;
   int64_t n_slots = 0;

@@ -80,7 +80,7 @@ def test_layout_host_sorted_and_consistent(kbf):
     s = g.integers(0, n_e, n_t).astype(np.int32)
     r = g.integers(0, n_r, n_t).astype(np.int32)
     o = g.integers(0, n_e, n_t).astype(np.int32)
-    specs = {0: (o, s, r, s, r), 1: (s, o, r, o, r), 2: (r, s, o, s, o)}
+    specs = {0: (o, r, s, s, r), 1: (s, r, o, o, r), 2: (r, s, o, o, s)}
     for which, (k1, k2, k3, ca_src, cb_src) in specs.items():
         off, ca, cb, perm = kbf.layout_host(s, r, o, n_e, n_r, which)
         assert sorted(perm.tolist()) == list(range(n_t))
