@@ -65,7 +65,7 @@ typedef enum {
  * Build a KB on the current HIP device from host triple arrays (Sec. 2.3: the
  * reified KB M_subj, M_obj, M_rel, one nonzero per row).
  *
- *   n_entities, n_relations : N_E >= 0 and N_R >= 0, each below 2^31.
+ *   n_entities, n_relations : 0 <= N_E, N_R <= 2^30.
  *   n_triples               : N_T, 0 <= N_T < 2^31.
  *   subj, rel, obj          : HOST int32 arrays of N_T ids (may be NULL when
  *                             N_T == 0); copied, the caller keeps ownership.
@@ -77,8 +77,9 @@ typedef enum {
  *
  * The three sorted layouts (by object, by subject, by relation) and their
  * work plans are built on the host and uploaded; the host copies are freed.
- * Device memory held: 16 bytes per triple per layout (48 per triple) plus
- * small plans.  Building takes seven stable counting passes over the triples.
+ * Device memory held: 8 bytes per triple per layout (24 per triple; 36 with
+ * weights) plus about 8 bytes per non-empty row per layout.  Building takes
+ * seven stable counting passes over the triples.
  * Errors: KB_EINVAL (sizes, null pointers), KB_ERANGE (an id out of range;
  * checked before any device work), KB_ENOMEM, KB_EHIP.
  */

@@ -32,7 +32,8 @@ kb_status hip_fail(hipError_t e, const char *what) {
 // Stream plan of one layout, resident on the device.
 struct DevLayout {
   int64_t rows = 0;
-  int4 *entries = nullptr;    // per position: (gathered id, second id, flush, weight bits)
+  int2 *entries = nullptr;    // the entry stream (triples and markers)
+  float *weights = nullptr;   // per entry, soft KB only
   int64_t n = 0;
   int32_t chunk = 0;
   int64_t n_chunks = 0;
@@ -66,11 +67,8 @@ int env_int(const char *name, int dflt) {
 struct kb_t {
   int device = 0;
   int n_cu = 0;
-  size_t lds_per_block = 0;
-  size_t lds_per_cu = 0;
   int64_t n_entities = 0, n_relations = 0, n_triples = 0;
   bool weighted = false;
-  int b_in_lds_mode = -1;  // -1 auto, 0 never, 1 whenever it fits
   DevLayout L[3];
   std::vector<void *> allocations;
   int64_t device_bytes = 0;
@@ -112,24 +110,17 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
                               int32_t fan_in, hipStream_t s) {
   PlanHost P = plan_layout(H, chunk, fan_in);
   D.rows = H.rows;
-  D.n = (int64_t)H.col_a.size();
+  D.n = (int64_t)P.entries.size();
   D.chunk = chunk;
   D.n_chunks = P.n_chunks;
   D.n_empty = (int64_t)P.empty_rows.size();
   D.n_slots = P.n_slots;
   D.n_split_rows = P.n_split_rows;
   D.max_row_len = P.max_row_len;
-  std::vector<int4> entries(D.n);
-  const bool wt = !H.weight.empty();
-  for (int64_t p = 0; p < D.n; ++p) {
-    float w = wt ? H.weight[p] : 1.0f;
-    int32_t wbits;
-    std::memcpy(&wbits, &w, sizeof wbits);
-    const int32_t a = H.col_a[p] | (P.run_end[p] ? INT32_MIN : 0);  // top bit: run ends here
-    entries[p] = make_int4(a, H.col_b[p], P.flush[p], wbits);
-  }
-  std::vector<int32_t>().swap(P.flush);
-  std::vector<uint8_t>().swap(P.run_end);
+  static_assert(sizeof(Entry) == sizeof(int2), "entry layout");
+  std::vector<int2> entries(D.n);
+  std::memcpy(entries.data(), P.entries.data(), D.n * sizeof(int2));
+  std::vector<Entry>().swap(P.entries);
   std::vector<int4> ctasks;
   D.level_begin.assign(1, 0);
   for (const auto &lv : P.levels) {
@@ -138,6 +129,7 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
   }
   kb_status st;
   if ((st = upload(kb, entries, &D.entries, s)) != KB_OK) return st;
+  if ((st = upload(kb, P.weights, &D.weights, s)) != KB_OK) return st;
   if ((st = upload(kb, P.empty_rows, &D.empty, s)) != KB_OK) return st;
   if ((st = upload(kb, ctasks, &D.ctasks, s)) != KB_OK) return st;
   // The host vectors die with this frame: wait for the copies first.
@@ -195,30 +187,13 @@ kb_status check_device(const kb_t *kb) {
 
 // Runs one pass: the stream kernel, the combine levels, the empty rows.
 kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float *A,
-                   const float *B, int64_t B_rows, bool b_may_use_lds, int32_t b, float *out,
+                   int64_t A_rows, const float *B, int64_t B_rows, int32_t b, float *out,
                    void *ws, hipStream_t s) {
   double *slots = static_cast<double *>(ws);
   {
     PhaseScope scope(kb, ph_base + 0, s);
-    StreamArgs a{D.entries, D.n, D.chunk, A, B, B_rows, b, out, slots};
-    bool lds = false;
-    int max_blocks = 0;
-    if (b_may_use_lds && kb->b_in_lds_mode != 0) {
-      const size_t bytes = stream_lds_bytes(b, B_rows);
-      const size_t limit = kb->b_in_lds_mode == 1
-                               ? kb->lds_per_block
-                               : std::min<size_t>(kb->lds_per_block, 64 * 1024);
-      if (bytes > 0 && bytes <= limit) {
-        lds = true;
-        const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(8, kb->lds_per_cu / bytes));
-        max_blocks = kb->n_cu * per_cu;
-        if (bytes > 64 * 1024) {
-          hipError_t e = prepare_stream_lds(b, bytes);
-          if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
-        }
-      }
-    }
-    hipError_t e = launch_stream(a, kb->weighted, lds, max_blocks, s);
+    StreamArgs a{D.entries, D.weights, D.n, D.chunk, A, A_rows, B, B_rows, b, out, slots};
+    hipError_t e = launch_stream(a, s);
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
   {
@@ -319,19 +294,13 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     int v = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, kb->device) == hipSuccess)
       kb->n_cu = v;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, kb->device) == hipSuccess)
-      kb->lds_per_block = (size_t)v;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, kb->device) == hipSuccess)
-      kb->lds_per_cu = (size_t)v;
-    if (kb->lds_per_cu < kb->lds_per_block) kb->lds_per_cu = kb->lds_per_block;
     if (kb->n_cu <= 0) kb->n_cu = 1;
-    kb->b_in_lds_mode = env_int("KBFOLLOW_B_IN_LDS", -1);
     kb->n_entities = n_entities;
     kb->n_relations = n_relations;
     kb->n_triples = n_triples;
     kb->weighted = weight != nullptr;
-    const int32_t chunk_seg = std::max(1, env_int("KBFOLLOW_CHUNK", 256));
-    const int32_t chunk_rel = std::max(1, env_int("KBFOLLOW_REL_CHUNK", 256));
+    const int32_t chunk_seg = std::max(2, env_int("KBFOLLOW_CHUNK", 256));
+    const int32_t chunk_rel = std::max(2, env_int("KBFOLLOW_REL_CHUNK", 256));
     const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
     {
       LayoutHost H[3];
@@ -409,8 +378,9 @@ kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, f
     if ((st = check_device(kb)) != KB_OK) return st;
     g_last_error.clear();
     if (!ent_bytes) return KB_OK;
-    return run_pass(kb, kb->L[BY_OBJ], KB_PH_FWD_STREAM, X, R, kb->n_relations, true, b, Y,
-                    workspace, static_cast<hipStream_t>(stream));
+    // By object, runs of equal relation: Y[o] = sum over runs of R[r] (.) sum of X[s].
+    return run_pass(kb, kb->L[BY_OBJ], KB_PH_FWD_STREAM, X, kb->n_entities, R, kb->n_relations,
+                    b, Y, workspace, static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(KB_EINVAL, "unexpected host error");
   }
@@ -446,14 +416,15 @@ kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const fl
     g_last_error.clear();
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (want_dx) {
-      st = run_pass(kb, kb->L[BY_SUBJ], KB_PH_DX_STREAM, dY, R, kb->n_relations, true, b, dX,
-                    workspace, s);
+      // By subject, runs of equal relation: dX[s] = sum over runs of R[r] (.) sum of dY[o].
+      st = run_pass(kb, kb->L[BY_SUBJ], KB_PH_DX_STREAM, dY, kb->n_entities, R, kb->n_relations,
+                    b, dX, workspace, s);
       if (st != KB_OK) return st;
     }
     if (want_dr) {
       // By relation, runs of equal subject: dR[k] = sum over runs of X[s] (.) sum of dY[o].
-      st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_STREAM, dY, X, kb->n_entities, false, b, dR,
-                    workspace, s);
+      st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_STREAM, dY, kb->n_entities, X, kb->n_entities,
+                    b, dR, workspace, s);
       if (st != KB_OK) return st;
     }
     return KB_OK;

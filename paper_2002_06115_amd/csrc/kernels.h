@@ -16,30 +16,28 @@ struct ColumnTiling {
 };
 ColumnTiling column_tiling(int32_t b);
 
-// Segmented gather-multiply-sum over a sorted triple stream (every pass of
-// the library).  entries[p] = (a, b_id, flush, weight bits) for position p;
-// lane group g walks positions [g * chunk, (g + 1) * chunk) accumulating
-//     acc += w[p] * A[a[p]] (.) B[b_id[p]]
-// and after position p writes acc to out row flush[p] (rounded to float) or
-// to workspace slot -(flush[p] + 1) (double) and restarts from zero, unless
-// flush[p] is kNoFlush.  B_rows is the row count of B; with b_in_lds the
-// workgroup first copies B's column slice into LDS.
+// Segmented gather-multiply-sum over one layout's entry stream (every pass
+// of the library).  entries[p] = (x, y): a triple x = a | run-end flag,
+// y = b_id, or a marker x = -1, y = target (row, -(slot + 1), or INT32_MIN
+// for none).  Lane group g walks entries [g * chunk, (g + 1) * chunk):
+//     run += w[p] * A[a]                      for every triple
+//     acc += run (.) B[b_id], run = 0         at a triple flagged run-end
+//     target = acc (float row / double slot), acc = 0   at a marker
+// A has A_rows rows and B has B_rows rows of b floats.
 struct StreamArgs {
-  const int4 *entries;
+  const int2 *entries;
+  const float *weights;  // per entry, nullptr for a hard KB
   int64_t n;
   int32_t chunk;
   const float *A;
+  int64_t A_rows;
   const float *B;
   int64_t B_rows;
   int32_t b;
   float *out;
   double *slots;
 };
-hipError_t launch_stream(const StreamArgs &a, bool weighted, bool b_in_lds, int max_blocks,
-                         hipStream_t s);
-
-// Bytes of LDS the stream kernel needs to hold B's column slice.
-size_t stream_lds_bytes(int32_t b, int64_t B_rows);
+hipError_t launch_stream(const StreamArgs &a, hipStream_t s);
 
 // Sums workspace slots in order (one combine level).
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int32_t b,
@@ -48,8 +46,5 @@ hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int
 // Writes +0.0 to the listed rows of out ([rows][b]).
 hipError_t launch_zero_rows(const int32_t *rows, int64_t n_rows, int32_t b, float *out,
                             hipStream_t s);
-
-// Lets the LDS variants of the stream kernel use `bytes` of dynamic LDS.
-hipError_t prepare_stream_lds(int32_t b, size_t bytes);
 
 }  // namespace kbf

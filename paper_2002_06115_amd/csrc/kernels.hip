@@ -29,6 +29,7 @@
 // rows per triple against two flops per element), so the double arithmetic
 // costs no time while it keeps long Zipf-hub rows accurate.
 #include "kernels.h"
+#include "plan.h"
 
 #include <climits>
 #include <utility>
@@ -136,69 +137,54 @@ __device__ __forceinline__ void store_slot(double *__restrict__ p, const double 
   }
 }
 
-// One lane group (LPT lanes) per chunk of the sorted triple stream; chunks
-// are visited grid-stride so a capped (persistent) grid works too.  Every
-// chunk holds the same number of positions, so the work is balanced whatever
-// the row lengths.
+// One lane group (LPT lanes) per chunk of the entry stream; chunks are
+// visited grid-stride so a capped (persistent) grid works too.  Every chunk
+// holds the same number of entries, so the work is balanced whatever the row
+// lengths.
 //
-// Inside a row the positions come in runs of equal B id.  The group sums the
-// A rows of a run (in double) and multiplies the sum by the B row once, at the
-// run's last position (entry.x has its top bit set there): B is read once per
-// run, not once per triple.  Where B comes from:
-//   kBBuffer : a raw buffer load per lane whose offset is out of range except
-//              at run ends, so the load never sits behind a branch and the
-//              lanes that need no B row generate no memory traffic;
-//   kBLds    : the workgroup first copies B's column slice into LDS (small
-//              tables only), lane-chunk j of row k kept at j ^ (k mod LPT) so
-//              the random rows of one wavefront spread over the banks;
-//   kBGlobal : a plain load of every position's B row (B of 4 GB or more).
-enum BSource { kBGlobal = 0, kBBuffer = 1, kBLds = 2 };
-
-template <int VEC, int LPT, int BSRC, bool WEIGHTED>
+// Inside a row the triples come in runs of equal B id.  The group sums the A
+// rows of a run (in double) and multiplies the sum by the B row once, at the
+// run's last triple: B is read once per run, not once per triple.
+//
+// With BUF (A and B each under 4 GB) both are read with raw buffer loads whose
+// offset is out of range where no row is needed (A at markers, B except at run
+// ends): such a lane returns zeros and generates no memory traffic, and no
+// load sits behind a branch.  Without BUF, plain loads read row 0 of A at
+// markers and every triple's B row.
+template <int VEC, int LPT, bool BUF, bool WEIGHTED>
 __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
-  constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
-  extern __shared__ float lds_b[];
   const int lane = threadIdx.x % LPT;
   const int grp = threadIdx.x / LPT;
-  const int col0 = blockIdx.y * W;
-  const int c = col0 + lane * VEC;
+  const int c = blockIdx.y * (LPT * VEC) + lane * VEC;
   const bool active = c < a.b;
   const size_t bb = (size_t)a.b;
+  // Lanes past b read column 0 and store nothing.
+  const int cl = active ? c : 0;
 
-  auto lds_chunk = [](int64_t k, int j) -> int64_t {
-    return k * W + (int64_t)((j ^ (int)(k & (LPT - 1))) * VEC);
-  };
-  if constexpr (BSRC == kBLds) {
-    const int64_t total = a.B_rows * W;
-    for (int64_t e = threadIdx.x; e < total; e += kBlock) {
-      const int64_t k = e / W;
-      const int col = (int)(e - k * W);
-      const int cc = col0 + col;
-      lds_b[lds_chunk(k, col / VEC) + col % VEC] = cc < a.b ? a.B[k * bb + cc] : 0.0f;
-    }
-    __syncthreads();
-  }
-  // (Only used with kBBuffer, where B is known to be under 4 GB.)
+  // (Only used with BUF, where A and B are known to be under 4 GB.)
+  const __amdgpu_buffer_rsrc_t arsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float *>(a.A), 0, (int)(uint32_t)(a.A_rows * a.b * sizeof(float)),
+      kRawBufferWord3);
   const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float *>(a.B), 0, (int)(uint32_t)(a.B_rows * a.b * sizeof(float)),
       kRawBufferWord3);
 
-  // Loads never sit behind a branch, so all kUnroll gathers of a step are in
-  // flight together: lanes past b read column 0 and store nothing, and the
-  // step past the end of a chunk re-reads its last position and adds nothing.
-  const int cl = active ? c : 0;
   const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
   const int64_t stride = (int64_t)gridDim.x * GPB;
 
   // Each lane loads K of a step's kUnroll entries (lane + k * LPT) and the
   // group shares them by broadcast, so one load instruction fetches the
-  // entries of every lane group in the wavefront.
+  // entries of every lane group in the wavefront.  A step past the end of a
+  // chunk re-reads its last entry and adds nothing.
   constexpr int K = (kUnroll + LPT - 1) / LPT;
-  auto fetch = [&](int64_t p, int64_t p1, int4 (&mine)[K]) {
+  auto fetch = [&](int64_t p, int64_t p1, int2 (&mine)[K], float (&wmine)[K]) {
 #pragma unroll
-    for (int k = 0; k < K; ++k)
-      mine[k] = a.entries[min(p + min(lane + k * LPT, kUnroll - 1), p1 - 1)];
+    for (int k = 0; k < K; ++k) {
+      const int64_t q = min(p + min(lane + k * LPT, kUnroll - 1), p1 - 1);
+      mine[k] = a.entries[q];
+      if constexpr (WEIGHTED) wmine[k] = a.weights[q];
+    }
   };
 
   for (int64_t g = (int64_t)blockIdx.x * GPB + grp; g < n_chunks; g += stride) {
@@ -210,56 +196,60 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
 
     // Software pipeline: the entries of the next step are loaded while this
     // step's gathers are in flight.
-    int4 mine_next[K];
-    fetch(p0, p1, mine_next);
+    int2 mine_next[K];
+    float wmine_next[K];
+    fetch(p0, p1, mine_next, wmine_next);
     for (int64_t p = p0; p < p1; p += kUnroll) {
       const int cnt = (int)min((int64_t)kUnroll, p1 - p);
-      int4 e[kUnroll];
+      int2 e[kUnroll];
+      float w[kUnroll];
       float xa[kUnroll][VEC], xb[kUnroll][VEC];
       static_for<kUnroll>([&](auto uc) {
         constexpr int u = decltype(uc)::value;
-        const int4 m = mine_next[u / LPT];
-        e[u] = make_int4(group_bcast<LPT, u % LPT>(m.x), group_bcast<LPT, u % LPT>(m.y),
-                         group_bcast<LPT, u % LPT>(m.z),
-                         WEIGHTED ? group_bcast<LPT, u % LPT>(m.w) : 0);
+        const int2 m = mine_next[u / LPT];
+        e[u] = make_int2(group_bcast<LPT, u % LPT>(m.x), group_bcast<LPT, u % LPT>(m.y));
+        if constexpr (WEIGHTED)
+          w[u] = __int_as_float(group_bcast<LPT, u % LPT>(__float_as_int(wmine_next[u / LPT])));
       });
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u)
-        load_row<VEC>(a.A + (size_t)(e[u].x & 0x7fffffff) * bb + cl, xa[u]);
-#pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        if constexpr (BSRC == kBBuffer) {
-          const uint32_t off =
-              e[u].x < 0 ? (uint32_t)(((size_t)e[u].y * bb + cl) * sizeof(float)) : kOutOfRange;
-          load_row_buffer<VEC>(brsrc, off, xb[u]);
-        } else if constexpr (BSRC == kBLds) {
-          load_row<VEC>(lds_b + lds_chunk(e[u].y, lane), xb[u]);
+        const bool triple = e[u].x >= 0;
+        const bool run_end = triple && (e[u].x & kRunEnd);
+        const size_t ia = triple ? (size_t)(e[u].x & kIdMask) : 0;
+        if constexpr (BUF) {
+          load_row_buffer<VEC>(arsrc, triple ? (uint32_t)((ia * bb + cl) * sizeof(float)) : kOutOfRange,
+                               xa[u]);
+          load_row_buffer<VEC>(brsrc,
+                               run_end ? (uint32_t)(((size_t)e[u].y * bb + cl) * sizeof(float))
+                                       : kOutOfRange,
+                               xb[u]);
         } else {
-          load_row<VEC>(a.B + (size_t)e[u].y * bb + cl, xb[u]);
+          load_row<VEC>(a.A + ia * bb + cl, xa[u]);
+          load_row<VEC>(a.B + (size_t)(triple ? e[u].y : 0) * bb + cl, xb[u]);
         }
       }
-      fetch(p + kUnroll, p1, mine_next);
+      fetch(p + kUnroll, p1, mine_next, wmine_next);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         if (u < cnt) {
-          if constexpr (WEIGHTED) {
-            const double w = (double)__int_as_float(e[u].w);
+          if (e[u].x >= 0) {
+            if constexpr (WEIGHTED) {
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) run[v] += w * (double)xa[u][v];
-          } else {
+              for (int v = 0; v < VEC; ++v) run[v] += (double)w[u] * (double)xa[u][v];
+            } else {
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) run[v] += (double)xa[u][v];
-          }
-          if (e[u].x < 0) {
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) {
-              acc[v] += run[v] * (double)xb[u][v];
-              run[v] = 0.0;
+              for (int v = 0; v < VEC; ++v) run[v] += (double)xa[u][v];
             }
-          }
-          const int f = e[u].z;
-          if (f != INT_MIN) {
-            if (active) {
+            if (e[u].x & kRunEnd) {
+#pragma unroll
+              for (int v = 0; v < VEC; ++v) {
+                acc[v] += run[v] * (double)xb[u][v];
+                run[v] = 0.0;
+              }
+            }
+          } else {
+            const int f = e[u].y;
+            if (active && f != INT_MIN) {
               if (f >= 0)
                 store_row<VEC>(a.out + (size_t)f * bb + c, acc);
               else
@@ -332,32 +322,27 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__rest
   }
 }
 
-template <int VEC, int BSRC, bool WT>
+template <int VEC, bool BUF, bool WT>
 const void *stream_fn(int lpt) {
   switch (lpt) {
-    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, BSRC, WT>);
-    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, BSRC, WT>);
-    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, BSRC, WT>);
-    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, BSRC, WT>);
-    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, BSRC, WT>);
-    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, BSRC, WT>);
-    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, BSRC, WT>);
+    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, BUF, WT>);
+    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, BUF, WT>);
+    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, BUF, WT>);
+    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, BUF, WT>);
+    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, BUF, WT>);
+    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, BUF, WT>);
+    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, BUF, WT>);
   }
   return nullptr;
 }
 
-template <int VEC>
-const void *stream_fn_vec(int lpt, int bsrc, bool wt) {
-  switch (bsrc) {
-    case kBGlobal: return wt ? stream_fn<VEC, kBGlobal, true>(lpt) : stream_fn<VEC, kBGlobal, false>(lpt);
-    case kBBuffer: return wt ? stream_fn<VEC, kBBuffer, true>(lpt) : stream_fn<VEC, kBBuffer, false>(lpt);
-    case kBLds: return wt ? stream_fn<VEC, kBLds, true>(lpt) : stream_fn<VEC, kBLds, false>(lpt);
+const void *stream_fn_for(const ColumnTiling &t, bool buf, bool wt) {
+  if (t.vec == 4) {
+    if (buf) return wt ? stream_fn<4, true, true>(t.lpt) : stream_fn<4, true, false>(t.lpt);
+    return wt ? stream_fn<4, false, true>(t.lpt) : stream_fn<4, false, false>(t.lpt);
   }
-  return nullptr;
-}
-
-const void *stream_fn_for(const ColumnTiling &t, int bsrc, bool wt) {
-  return t.vec == 4 ? stream_fn_vec<4>(t.lpt, bsrc, wt) : stream_fn_vec<1>(t.lpt, bsrc, wt);
+  if (buf) return wt ? stream_fn<1, true, true>(t.lpt) : stream_fn<1, true, false>(t.lpt);
+  return wt ? stream_fn<1, false, true>(t.lpt) : stream_fn<1, false, false>(t.lpt);
 }
 
 template <int VEC>
@@ -395,38 +380,20 @@ ColumnTiling column_tiling(int32_t b) {
   return t;
 }
 
-size_t stream_lds_bytes(int32_t b, int64_t B_rows) {
-  const ColumnTiling t = column_tiling(b);
-  return (size_t)B_rows * (size_t)t.width * sizeof(float);
-}
-
-hipError_t prepare_stream_lds(int32_t b, size_t bytes) {
-  const ColumnTiling t = column_tiling(b);
-  for (bool wt : {false, true}) {
-    const void *fn = stream_fn_for(t, kBLds, wt);
-    if (!fn) return hipErrorInvalidValue;
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-hipError_t launch_stream(const StreamArgs &a, bool weighted, bool b_in_lds, int max_blocks,
-                         hipStream_t s) {
+hipError_t launch_stream(const StreamArgs &a, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(a.b);
-  // Raw-buffer offsets are 32-bit: B of 4 GB or more takes plain loads.
-  const bool fits = (uint64_t)a.B_rows * (uint64_t)a.b * sizeof(float) <= (uint64_t)kOutOfRange;
-  const int bsrc = b_in_lds ? kBLds : (fits ? kBBuffer : kBGlobal);
-  const void *fn = stream_fn_for(t, bsrc, weighted);
+  // Raw-buffer offsets are 32-bit: tables of 4 GB or more take plain loads.
+  const uint64_t row_bytes = (uint64_t)a.b * sizeof(float);
+  const bool buf = (uint64_t)a.A_rows * row_bytes <= (uint64_t)kOutOfRange &&
+                   (uint64_t)a.B_rows * row_bytes <= (uint64_t)kOutOfRange;
+  const void *fn = stream_fn_for(t, buf, a.weights != nullptr);
   if (!fn) return hipErrorInvalidValue;
   const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
-  const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, max_blocks),
-                  (unsigned)t.n_slices);
-  const size_t lds = b_in_lds ? stream_lds_bytes(a.b, a.B_rows) : 0;
+  const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
   StreamArgs arg = a;
   void *params[] = {&arg};
-  return hipLaunchKernel(fn, grid, dim3(kBlock), params, lds, s);
+  return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int32_t b,

@@ -21,8 +21,8 @@ std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_
   char msg[160];
   if (n_entities < 0 || n_relations < 0 || n_triples < 0)
     return "n_entities, n_relations and n_triples must be >= 0";
-  if (n_entities > INT32_MAX || n_relations > INT32_MAX)
-    return "n_entities and n_relations must be below 2^31";
+  if (n_entities > (1 << 30) || n_relations > (1 << 30))
+    return "n_entities and n_relations must be at most 2^30";
   if (n_triples > INT32_MAX) return "n_triples must be below 2^31";
   if (n_triples > 0 && (!subj || !rel || !obj)) return "subj, rel and obj must be non-NULL";
   for (int64_t l = 0; l < n_triples; ++l) {
@@ -103,10 +103,14 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
   PlanHost P;
   P.chunk = chunk;
   P.fan_in = fan_in;
-  const int64_t n = (int64_t)L.col_a.size();
-  P.n_chunks = (n + chunk - 1) / chunk;
-  P.flush.assign(n, kNoFlush);
-  P.run_end.assign(n, 0);
+  const bool weighted = !L.weight.empty();
+  std::vector<Entry> &S = P.entries;
+  S.reserve(L.col_a.size() + L.rows + L.col_a.size() / std::max(1, chunk - 1) + 2);
+  if (weighted) P.weights.reserve(S.capacity());
+  auto marker = [&](int32_t target) {
+    S.push_back({kMarker, target});
+    if (weighted) P.weights.push_back(0.0f);
+  };
   struct Split {
     int32_t row;
     int64_t first, n;
@@ -119,22 +123,38 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
       P.empty_rows.push_back((int32_t)q);
       continue;
     }
-    for (int64_t p = beg; p < end; ++p)
-      P.run_end[p] = (p + 1 == end || (p + 1) % chunk == 0 || L.col_b[p + 1] != L.col_b[p]);
-    const int64_t c0 = beg / chunk, c1 = (end - 1) / chunk;
-    if (c0 == c1) {
-      P.flush[end - 1] = (int32_t)q;
-      continue;
+    int64_t first_slot = -1, n_slots = 0;
+    bool pending = false;  // triples of this row since the last marker
+    for (int64_t p = beg; p < end; ++p) {
+      if ((int64_t)S.size() % chunk == chunk - 1) {
+        // The chunk's last entry must be a marker.
+        if (pending) {
+          S.back().x |= kRunEnd;  // fold the open run before the partial is written
+          if (n_slots == 0) first_slot = P.n_slots;
+          marker(-(int32_t)P.n_slots - 1);
+          ++P.n_slots;
+          ++n_slots;
+        } else {
+          marker(kNoTarget);
+        }
+        pending = false;
+      }
+      const bool run_end = p + 1 == end || L.col_b[p + 1] != L.col_b[p];
+      S.push_back({L.col_a[p] | (run_end ? kRunEnd : 0), L.col_b[p]});
+      if (weighted) P.weights.push_back(L.weight[p]);
+      pending = true;
     }
-    const int64_t np = c1 - c0 + 1;
-    for (int64_t k = 0; k < np; ++k) {
-      const int64_t last = std::min(end, (c0 + k + 1) * chunk) - 1;
-      P.flush[last] = (int32_t)(-(P.n_slots + k) - 1);
+    if (n_slots > 0) {
+      marker(-(int32_t)P.n_slots - 1);
+      ++P.n_slots;
+      ++n_slots;
+      splits.push_back({(int32_t)q, first_slot, n_slots});
+      ++P.n_split_rows;
+    } else {
+      marker((int32_t)q);
     }
-    splits.push_back({(int32_t)q, P.n_slots, np});
-    P.n_slots += np;
-    ++P.n_split_rows;
   }
+  P.n_chunks = ((int64_t)S.size() + chunk - 1) / chunk;
   // Combine levels: a row split into n partials is reduced fan_in slots at a
   // time until one task writes the row.
   for (const Split &s : splits) {

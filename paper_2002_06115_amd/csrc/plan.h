@@ -8,12 +8,8 @@
 //   backward dX : rows = subjects,  sum over r-runs of R[r] (.) sum dY[o]
 //   backward dR : rows = relations, sum over s-runs of X[s] (.) sum dY[o]
 // so the planner sorts the triples three ways (counting sorts, stable) and
-// cuts the sorted list into equal chunks, one per lane group, whatever the
-// row lengths (Zipf hubs and one-triple rows alike).  A row inside one chunk
-// is written directly by the lane group that sums it; a row that crosses chunk
-// boundaries writes one double-precision partial per chunk into a workspace
-// slot and the partials are added up in chunk order by combine tasks, at most
-// `fan_in` slots per task, over as many levels as the row needs.
+// turns each sorted list into a stream of 8-byte entries cut into equal
+// chunks (see PlanHost).
 #pragma once
 
 #include <climits>
@@ -24,9 +20,6 @@
 namespace kbf {
 
 enum LayoutKind { BY_OBJ = 0, BY_SUBJ = 1, BY_REL = 2 };
-
-// Marks a position whose running sum is not written out.
-constexpr int32_t kNoFlush = INT32_MIN;
 
 // Sum slots [first, first + n) in order into dst (row if >= 0, else slot -(dst + 1)).
 struct CombineTask {
@@ -42,21 +35,35 @@ struct LayoutHost {
   std::vector<int32_t> perm;      // caller index of the triple at each position
 };
 
-// The stream plan of one layout: the sorted positions are cut into chunks of
-// `chunk` consecutive positions, one chunk per lane group.  flush[p] says what
-// the lane group does after adding position p: nothing (kNoFlush), write the
-// row it just finished (>= 0), or write its partial sum of a row that crosses
-// a chunk boundary to workspace slot -(flush[p] + 1).  A row's partials are
-// numbered in chunk order and summed in that order by the combine levels.
-// Inside a row the positions form runs of equal col_b; run_end[p] marks the
-// last position of a run (a row end or chunk end also ends a run), where the
-// kernel multiplies the run's sum of A rows by the B row once.
+// One 8-byte stream entry.  A triple: x = (id gathered for this triple, col_a)
+// | kRunEnd when it is the last triple of a run of equal col_b, y = col_b.  A
+// marker (x = kMarker): write the running sum to y -- a row (y >= 0), a
+// workspace slot -(y + 1), or nothing (y = kNoTarget) -- and restart from zero.
+struct Entry {
+  int32_t x, y;
+};
+constexpr int32_t kMarker = -1;
+constexpr int32_t kRunEnd = 1 << 30;
+constexpr int32_t kIdMask = kRunEnd - 1;
+constexpr int32_t kNoTarget = INT32_MIN;
+
+// The stream plan of one layout.  The sorted triples of every non-empty row
+// are followed by a marker that writes the row, and the stream is cut into
+// chunks of `chunk` entries, one chunk per lane group, whatever the row
+// lengths (Zipf hubs and one-triple rows alike).  The last entry of every
+// chunk is a marker: where a row continues past it, that marker writes the
+// chunk's partial sum of the row to a workspace slot, and the row's final
+// marker writes its last partial to a slot too.  A row's slots are numbered
+// consecutively in chunk order and summed in that order by combine tasks, at
+// most `fan_in` slots per task, over as many levels as the row needs.
+// Inside a row the triples form runs of equal col_b; the kernel multiplies a
+// run's summed A rows by its B row once, at the entry flagged kRunEnd.
 struct PlanHost {
   int32_t chunk = 0;
   int32_t fan_in = 0;
   int64_t n_chunks = 0;
-  std::vector<int32_t> flush;      // per position
-  std::vector<uint8_t> run_end;    // per position: last of a run of equal col_b (or of a chunk)
+  std::vector<Entry> entries;
+  std::vector<float> weights;       // per entry (markers 0), empty for a hard KB
   std::vector<int32_t> empty_rows;
   std::vector<std::vector<CombineTask>> levels;
   int64_t n_slots = 0;

@@ -126,3 +126,28 @@ def test_argument_errors(kbf):
     torch.cuda.synchronize()
     with pytest.raises(ValueError):
         kb.follow(X, torch.zeros((3, 7), device="cuda"))
+
+
+@pytest.mark.parametrize("chunk,fan_in", [(2, 2), (3, 32), (5, 3), (8, 2), (9, 4), (64, 2), (4096, 32)])
+def test_chunk_and_combine_plans(kbf, chunk, fan_in, monkeypatch):
+    # Tiny chunks put a marker every few entries: runs cut by chunk ends,
+    # no-op markers, rows split into many slots, deep combine trees.
+    monkeypatch.setenv("KBFOLLOW_CHUNK", str(chunk))
+    monkeypatch.setenv("KBFOLLOW_REL_CHUNK", str(chunk))
+    monkeypatch.setenv("KBFOLLOW_FAN_IN", str(fan_in))
+    n_e, n_r = 300, 4
+    g = np.random.default_rng(chunk * 100 + fan_in)
+    s = np.concatenate([g.integers(0, n_e, 3000), np.full(700, 5)]).astype(np.int32)
+    r = g.integers(0, n_r, len(s)).astype(np.int32)
+    o = np.concatenate([g.integers(0, n_e, 3000), g.integers(0, 3, 700)]).astype(np.int32)
+    for b, exact in ((4, True), (12, False), (7, False)):
+        if exact:
+            X = (g.random((b, n_e)) < 0.2).astype(np.float32)
+            R = np.zeros((b, n_r), np.float32)
+            R[np.arange(b), g.integers(0, n_r, b)] = 1.0
+            dY = np.ones((b, n_e), np.float32)
+        else:
+            X, R, dY = rand_io(b + chunk, b, n_e, n_r)
+        kb = both(kbf, s, r, o, n_e, n_r, X, R, dY, exact, f"chunk={chunk} fan_in={fan_in} b={b}")
+    info = kb.info()
+    assert info["chunk_len"] == [chunk, chunk, chunk]
