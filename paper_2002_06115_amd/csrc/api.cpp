@@ -299,8 +299,17 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     kb->n_relations = n_relations;
     kb->n_triples = n_triples;
     kb->weighted = weight != nullptr;
-    const int32_t chunk_seg = std::max(2, env_int("KBFOLLOW_CHUNK", 256));
-    const int32_t chunk_rel = std::max(2, env_int("KBFOLLOW_REL_CHUNK", 256));
+    // Chunk length: 256 entries, shorter for small streams so that there are
+    // at least ~32 K chunks to spread over the GPU (never below 16).
+    auto default_chunk = [](int64_t entries) {
+      int32_t c = 256;
+      while (c > 16 && entries / c < 32768) c /= 2;
+      return c;
+    };
+    const int32_t chunk_seg =
+        std::max(2, env_int("KBFOLLOW_CHUNK", default_chunk(n_triples + n_entities)));
+    const int32_t chunk_rel =
+        std::max(2, env_int("KBFOLLOW_REL_CHUNK", default_chunk(n_triples + n_relations)));
     const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
     {
       LayoutHost H[3];
