@@ -69,6 +69,7 @@ struct kb_t {
   int n_cu = 0;
   int64_t n_entities = 0, n_relations = 0, n_triples = 0;
   bool weighted = false;
+  bool plain_loads = false;  // force plain loads instead of raw buffer loads (testing)
   DevLayout L[3];
   std::vector<void *> allocations;
   int64_t device_bytes = 0;
@@ -193,7 +194,7 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
   {
     PhaseScope scope(kb, ph_base + 0, s);
     StreamArgs a{D.entries, D.weights, D.n, D.chunk, A, A_rows, B, B_rows, b, out, slots};
-    hipError_t e = launch_stream(a, s);
+    hipError_t e = launch_stream(a, kb->plain_loads, s);
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
   {
@@ -295,6 +296,7 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, kb->device) == hipSuccess)
       kb->n_cu = v;
     if (kb->n_cu <= 0) kb->n_cu = 1;
+    kb->plain_loads = env_int("KBFOLLOW_PLAIN_LOADS", 0) != 0;
     kb->n_entities = n_entities;
     kb->n_relations = n_relations;
     kb->n_triples = n_triples;

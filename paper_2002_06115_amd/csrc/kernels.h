@@ -37,7 +37,9 @@ struct StreamArgs {
   float *out;
   double *slots;
 };
-hipError_t launch_stream(const StreamArgs &a, hipStream_t s);
+// plain_loads forces the plain-load variant (used anyway for tables of 4 GB
+// or more) so it can be tested at small sizes.
+hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s);
 
 // Sums workspace slots in order (one combine level).
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int32_t b,

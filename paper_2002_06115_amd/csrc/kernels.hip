@@ -380,12 +380,12 @@ ColumnTiling column_tiling(int32_t b) {
   return t;
 }
 
-hipError_t launch_stream(const StreamArgs &a, hipStream_t s) {
+hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(a.b);
   // Raw-buffer offsets are 32-bit: tables of 4 GB or more take plain loads.
   const uint64_t row_bytes = (uint64_t)a.b * sizeof(float);
-  const bool buf = (uint64_t)a.A_rows * row_bytes <= (uint64_t)kOutOfRange &&
+  const bool buf = !plain_loads && (uint64_t)a.A_rows * row_bytes <= (uint64_t)kOutOfRange &&
                    (uint64_t)a.B_rows * row_bytes <= (uint64_t)kOutOfRange;
   const void *fn = stream_fn_for(t, buf, a.weights != nullptr);
   if (!fn) return hipErrorInvalidValue;

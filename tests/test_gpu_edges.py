@@ -151,3 +151,17 @@ def test_chunk_and_combine_plans(kbf, chunk, fan_in, monkeypatch):
         kb = both(kbf, s, r, o, n_e, n_r, X, R, dY, exact, f"chunk={chunk} fan_in={fan_in} b={b}")
     info = kb.info()
     assert info["chunk_len"] == [chunk, chunk, chunk]
+
+
+@pytest.mark.parametrize("b", [4, 32, 33, 256])
+def test_plain_load_path(kbf, b, monkeypatch):
+    # Tables of 4 GB or more are read with plain loads instead of raw buffer
+    # loads; force that path at a small size.
+    monkeypatch.setenv("KBFOLLOW_PLAIN_LOADS", "1")
+    n_e, n_r = 2000, 7
+    s, r, o = rand_kb(50 + b, n_e, n_r, 20_000)
+    s[:3000] = 9                       # a hub, split across chunks
+    X, R, dY = rand_io(50 + b, b, n_e, n_r)
+    both(kbf, s, r, o, n_e, n_r, X, R, dY, False, f"plain loads b={b}")
+    wt = np.random.default_rng(b).uniform(0.5, 1.5, len(s)).astype(np.float32)
+    both(kbf, s, r, o, n_e, n_r, X, R, dY, False, f"plain loads weighted b={b}", weight=wt)
