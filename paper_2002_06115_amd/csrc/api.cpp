@@ -308,10 +308,14 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
       while (c > 16 && entries / c < 32768) c /= 2;
       return c;
     };
+    // A chunk is a whole number of kernel steps.
+    auto whole_steps = [](int32_t c) {
+      return std::max(kChunkQuantum, (c + kChunkQuantum - 1) / kChunkQuantum * kChunkQuantum);
+    };
     const int32_t chunk_seg =
-        std::max(2, env_int("KBFOLLOW_CHUNK", default_chunk(n_triples + n_entities)));
+        whole_steps(env_int("KBFOLLOW_CHUNK", default_chunk(n_triples + n_entities)));
     const int32_t chunk_rel =
-        std::max(2, env_int("KBFOLLOW_REL_CHUNK", default_chunk(n_triples + n_relations)));
+        whole_steps(env_int("KBFOLLOW_REL_CHUNK", default_chunk(n_triples + n_relations)));
     const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
     {
       LayoutHost H[3];

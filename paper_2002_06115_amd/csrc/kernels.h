@@ -16,10 +16,14 @@ struct ColumnTiling {
 };
 ColumnTiling column_tiling(int32_t b);
 
+// Chunk lengths must be multiples of this (the kernel's step, kUnroll entries).
+constexpr int32_t kChunkQuantum = 8;
+
 // Segmented gather-multiply-sum over one layout's entry stream (every pass
 // of the library).  entries[p] = (x, y): a triple x = a | run-end flag,
 // y = b_id, or a marker x = -1, y = target (row, -(slot + 1), or INT32_MIN
-// for none).  Lane group g walks entries [g * chunk, (g + 1) * chunk):
+// for none); n is a multiple of chunk, and chunk of kChunkQuantum.  Lane
+// group g walks entries [g * chunk, (g + 1) * chunk):
 //     run += w[p] * A[a]                      for every triple
 //     acc += run (.) B[b_id], run = 0         at a triple flagged run-end
 //     target = acc (float row / double slot), acc = 0   at a marker

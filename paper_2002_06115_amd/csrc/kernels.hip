@@ -38,12 +38,9 @@ namespace kbf {
 
 namespace {
 
-#ifndef KBF_UNROLL
-#define KBF_UNROLL 8
-#endif
-
-constexpr int kBlock = 256;         // threads per workgroup (4 wavefronts of 64)
-constexpr int kUnroll = KBF_UNROLL; // triples whose loads a lane group keeps in flight
+constexpr int kBlock = 256;   // threads per workgroup (4 wavefronts of 64)
+constexpr int kUnroll = 8;    // entries per step; a lane group keeps their loads in flight
+static_assert(kChunkQuantum % kUnroll == 0, "a chunk is a whole number of steps");
 
 // Buffer-resource word 3 for gfx9-family raw buffers, and an offset past any
 // buffer this library makes: such a load returns zeros without touching memory.
@@ -103,13 +100,17 @@ __device__ __forceinline__ void load_row_buffer(__amdgpu_buffer_rsrc_t rsrc, uin
   }
 }
 
+typedef float native_float4 __attribute__((ext_vector_type(4)));
+
+// Output rows are written once and not read again by the pass: non-temporal
+// stores keep them from displacing gathered rows in the caches.
 template <int VEC>
 __device__ __forceinline__ void store_row(float *__restrict__ p, const double (&acc)[VEC]) {
   if constexpr (VEC == 4) {
-    *reinterpret_cast<float4 *>(p) =
-        make_float4((float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]);
+    const native_float4 v = {(float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]};
+    __builtin_nontemporal_store(v, reinterpret_cast<native_float4 *>(p));
   } else {
-    *p = (float)acc[0];
+    __builtin_nontemporal_store((float)acc[0], p);
   }
 }
 
@@ -170,18 +171,19 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
       const_cast<float *>(a.B), 0, (int)(uint32_t)(a.B_rows * a.b * sizeof(float)),
       kRawBufferWord3);
 
-  const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
+  const int64_t n_chunks = a.n / a.chunk;
   const int64_t stride = (int64_t)gridDim.x * GPB;
 
   // Each lane loads K of a step's kUnroll entries (lane + k * LPT) and the
   // group shares them by broadcast, so one load instruction fetches the
-  // entries of every lane group in the wavefront.  A step past the end of a
-  // chunk re-reads its last entry and adds nothing.
+  // entries of every lane group in the wavefront.  (The prefetch after a
+  // chunk's last step reads the next chunk's first entries, or the stream's
+  // last entry at its end, and is not used.)
   constexpr int K = (kUnroll + LPT - 1) / LPT;
-  auto fetch = [&](int64_t p, int64_t p1, int2 (&mine)[K], float (&wmine)[K]) {
+  auto fetch = [&](int64_t p, int2 (&mine)[K], float (&wmine)[K]) {
 #pragma unroll
     for (int k = 0; k < K; ++k) {
-      const int64_t q = min(p + min(lane + k * LPT, kUnroll - 1), p1 - 1);
+      const int64_t q = min(p + min(lane + k * LPT, kUnroll - 1), a.n - 1);
       mine[k] = a.entries[q];
       if constexpr (WEIGHTED) wmine[k] = a.weights[q];
     }
@@ -189,7 +191,7 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
 
   for (int64_t g = (int64_t)blockIdx.x * GPB + grp; g < n_chunks; g += stride) {
     const int64_t p0 = g * a.chunk;
-    const int64_t p1 = min(p0 + (int64_t)a.chunk, a.n);
+    const int64_t p1 = p0 + a.chunk;
     double acc[VEC], run[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] = run[v] = 0.0;
@@ -198,9 +200,8 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
     // step's gathers are in flight.
     int2 mine_next[K];
     float wmine_next[K];
-    fetch(p0, p1, mine_next, wmine_next);
+    fetch(p0, mine_next, wmine_next);
     for (int64_t p = p0; p < p1; p += kUnroll) {
-      const int cnt = (int)min((int64_t)kUnroll, p1 - p);
       int2 e[kUnroll];
       float w[kUnroll];
       float xa[kUnroll][VEC], xb[kUnroll][VEC];
@@ -228,37 +229,34 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
           load_row<VEC>(a.B + (size_t)(triple ? e[u].y : 0) * bb + cl, xb[u]);
         }
       }
-      fetch(p + kUnroll, p1, mine_next, wmine_next);
+      fetch(p + kUnroll, mine_next, wmine_next);
+      // Branch-free accumulation: selects, not branches, decide what an entry
+      // does (a select also keeps an Inf or NaN row from leaking into a sum it
+      // does not belong to, as a multiply by zero would); only the store of a
+      // marker is predicated.
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        if (u < cnt) {
-          if (e[u].x >= 0) {
-            if constexpr (WEIGHTED) {
+        const bool triple = e[u].x >= 0;
+        const bool run_end = triple && (e[u].x & kRunEnd);
 #pragma unroll
-              for (int v = 0; v < VEC; ++v) run[v] += (double)w[u] * (double)xa[u][v];
-            } else {
-#pragma unroll
-              for (int v = 0; v < VEC; ++v) run[v] += (double)xa[u][v];
-            }
-            if (e[u].x & kRunEnd) {
-#pragma unroll
-              for (int v = 0; v < VEC; ++v) {
-                acc[v] += run[v] * (double)xb[u][v];
-                run[v] = 0.0;
-              }
-            }
-          } else {
-            const int f = e[u].y;
-            if (active && f != INT_MIN) {
-              if (f >= 0)
-                store_row<VEC>(a.out + (size_t)f * bb + c, acc);
-              else
-                store_slot<VEC>(a.slots + (size_t)(-(f + 1)) * bb + c, acc);
-            }
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[v] = 0.0;
-          }
+        for (int v = 0; v < VEC; ++v) {
+          double t = (double)xa[u][v];
+          if constexpr (WEIGHTED) t *= (double)w[u];
+          // (Buffer loads already return exact zeros at markers.)
+          run[v] += (BUF || triple) ? t : 0.0;
+          const double closed = acc[v] + run[v] * (double)xb[u][v];
+          acc[v] = run_end ? closed : acc[v];
+          run[v] = run_end ? 0.0 : run[v];
         }
+        const int f = e[u].y;
+        if (!triple && active && f != INT_MIN) {
+          if (f >= 0)
+            store_row<VEC>(a.out + (size_t)f * bb + c, acc);
+          else
+            store_slot<VEC>(a.slots + (size_t)(-(f + 1)) * bb + c, acc);
+        }
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[v] = triple ? acc[v] : 0.0;
       }
     }
   }
@@ -389,7 +387,8 @@ hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
                    (uint64_t)a.B_rows * row_bytes <= (uint64_t)kOutOfRange;
   const void *fn = stream_fn_for(t, buf, a.weights != nullptr);
   if (!fn) return hipErrorInvalidValue;
-  const int64_t n_chunks = (a.n + a.chunk - 1) / a.chunk;
+  if (a.chunk % kChunkQuantum != 0 || a.n % a.chunk != 0) return hipErrorInvalidValue;
+  const int64_t n_chunks = a.n / a.chunk;
   const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
   StreamArgs arg = a;
   void *params[] = {&arg};

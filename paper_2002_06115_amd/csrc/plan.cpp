@@ -154,7 +154,10 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
       marker((int32_t)q);
     }
   }
-  P.n_chunks = ((int64_t)S.size() + chunk - 1) / chunk;
+  // Pad with no-op markers to whole chunks: every lane group then walks
+  // exactly `chunk` entries.
+  while ((int64_t)S.size() % chunk != 0) marker(kNoTarget);
+  P.n_chunks = (int64_t)S.size() / chunk;
   // Combine levels: a row split into n partials is reduced fan_in slots at a
   // time until one task writes the row.
   for (const Split &s : splits) {
