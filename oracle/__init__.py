@@ -9,8 +9,11 @@ nothing from the product.
   one rounding to float), in the paper's batch-major orientation ``[b][N]``.
 * :func:`follow_f64`, :func:`follow_backward_f64` -- the same sums kept in
   double, for multi-hop chains.
+* :func:`follow_residual`, :func:`follow_backward_residual` -- the residual hop
+  of the KB-completion chains (Sec. 3.2, App. E): follow(X, R) + gamma * X.
 * :mod:`oracle.chain` -- the three-hop chain with its softmax, L1 normalisation
-  and cross-entropy loss, forward and backward, in double.
+  and cross-entropy loss, and the residual chain, forward and backward, in
+  double.
 """
 from __future__ import annotations
 
@@ -48,8 +51,13 @@ def _load():
         lib.ora_sampled.argtypes = [i32, i64, i64, i64, p, p, p, p, i32, p, p, p, i32, p, p, i32]
         lib.ora_follow_f64.argtypes = [i64, i64, i64, p, p, p, p, i32, p, p, p]
         lib.ora_follow_backward_f64.argtypes = [i64, i64, i64, p, p, p, p, i32, p, p, p, p, p]
+        f32 = ctypes.c_float
+        lib.ora_follow_residual.argtypes = [i64, i64, i64, p, p, p, p, i32, p, p, f32, p, i32]
+        lib.ora_follow_backward_residual.argtypes = [i64, i64, i64, p, p, p, p, i32, p, p, p, f32,
+                                                     p, p, i32]
         for f in (lib.ora_follow, lib.ora_follow_backward, lib.ora_sampled, lib.ora_follow_f64,
-                  lib.ora_follow_backward_f64):
+                  lib.ora_follow_backward_f64, lib.ora_follow_residual,
+                  lib.ora_follow_backward_residual):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -145,4 +153,34 @@ def follow_backward_f64(subj, rel, obj, n_entities, n_relations, X, R, dY, weigh
                                          _ptr(rel), _ptr(obj), _ptr(weight), b, _ptr(X), _ptr(R),
                                          _ptr(dY), _ptr(dX), _ptr(dR))
     _check(rc, "follow_backward_f64")
+    return dX, dR
+
+
+def follow_residual(subj, rel, obj, n_entities, n_relations, X, R, gamma=1.0, weight=None,
+                    nthreads=0):
+    """Y = follow(X, R) + gamma * X, rounded to float once."""
+    subj, rel, obj = _ids(subj), _ids(rel), _ids(obj)
+    X, R, weight = _f32(X), _f32(R), _f32(weight)
+    b = X.shape[0]
+    Y = np.empty((b, n_entities), np.float32)
+    rc = _load().ora_follow_residual(n_entities, n_relations, len(subj), _ptr(subj), _ptr(rel),
+                                     _ptr(obj), _ptr(weight), b, _ptr(X), _ptr(R), gamma,
+                                     _ptr(Y), nthreads)
+    _check(rc, "follow_residual")
+    return Y
+
+
+def follow_backward_residual(subj, rel, obj, n_entities, n_relations, X, R, dY, gamma=1.0,
+                             weight=None, nthreads=0):
+    """(dX, dR) of the residual hop: dX = follow's dX + gamma * dY."""
+    subj, rel, obj = _ids(subj), _ids(rel), _ids(obj)
+    X, R, dY, weight = _f32(X), _f32(R), _f32(dY), _f32(weight)
+    b = dY.shape[0]
+    dX = np.empty((b, n_entities), np.float32)
+    dR = np.empty((b, n_relations), np.float32)
+    rc = _load().ora_follow_backward_residual(n_entities, n_relations, len(subj), _ptr(subj),
+                                              _ptr(rel), _ptr(obj), _ptr(weight), b, _ptr(X),
+                                              _ptr(R), _ptr(dY), gamma, _ptr(dX), _ptr(dR),
+                                              nthreads)
+    _check(rc, "follow_backward_residual")
     return dX, dR

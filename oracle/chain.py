@@ -1,4 +1,4 @@
-"""Three-hop chain oracle, in double precision (test infrastructure only).
+"""Multi-hop chain oracles, in double precision (test infrastructure only).
 
 The multi-hop KBQA model of Sec. 3.2 chains follow steps,
 x^t = follow(x^{t-1}, r^t) for t = 1..T, then takes a softmax of x^T and a
@@ -70,3 +70,34 @@ def chain_grad(kb_arrays, n_entities, n_relations, x0, rho, target):
         drho[t - 1] = r * (dr - (dr * r).sum(axis=1, keepdims=True))
         dx = dxp
     return loss, dx, drho
+
+
+# ---------------------------------------------------------------------------
+# Residual chains of the KB-completion model (Sec. 3.2, App. E):
+#   x^t = follow(x^{t-1}, r^t) + x^{t-1},  t = 1..T.
+# Backward for a loss with upstream G = dL/dx^T (chain rule):
+#   dx^T = G;  dr^t = follow's dR at (x^{t-1}, r^t) with upstream dx^t;
+#   dx^{t-1} = follow's dX at r^t with upstream dx^t, plus dx^t.
+# ---------------------------------------------------------------------------
+
+def residual_chain(kb_arrays, n_entities, n_relations, x0, rs, weight=None):
+    """[x^0, x^1, ..., x^T] for relation sets rs = [r^1..r^T] (each [b][N_R])."""
+    subj, rel, obj = kb_arrays
+    xs = [np.asarray(x0, np.float64)]
+    for r in rs:
+        xs.append(follow_f64(subj, rel, obj, n_entities, n_relations, xs[-1], r, weight) + xs[-1])
+    return xs
+
+
+def residual_chain_grad(kb_arrays, n_entities, n_relations, x0, rs, G, weight=None):
+    """(dL/dx^0, [dL/dr^1..dL/dr^T]) for upstream G = dL/dx^T."""
+    subj, rel, obj = kb_arrays
+    xs = residual_chain(kb_arrays, n_entities, n_relations, x0, rs, weight)
+    dx = np.asarray(G, np.float64)
+    drs = [None] * len(rs)
+    for t in range(len(rs), 0, -1):
+        dxp, dr = follow_backward_f64(subj, rel, obj, n_entities, n_relations, xs[t - 1],
+                                      rs[t - 1], dx, weight)
+        drs[t - 1] = dr
+        dx = dxp + dx
+    return dx, drs

@@ -257,3 +257,74 @@ int ora_follow_backward_f64(int64_t n_e, int64_t n_r, int64_t n_t, const int32_t
   }
   return ORA_OK;
 }
+
+/*
+ * Residual follow, the hop of the KB-completion chains (Sec. 3.2, App. E):
+ *   Y[beta][j]  = follow(X, R)[beta][j] + gamma * X[beta][j]
+ * and its backward for upstream dY:
+ *   dX[beta][i] = (gradient of follow w.r.t. X)[beta][i] + gamma * dY[beta][i]
+ *   dR          = gradient of follow w.r.t. R (the residual term has none).
+ * The per-triple sum is taken first (caller order, double), then gamma * X
+ * (or gamma * dY) is added in double and the result rounded to float once.
+ */
+int ora_follow_residual(int64_t n_e, int64_t n_r, int64_t n_t, const int32_t *subj,
+                        const int32_t *rel, const int32_t *obj, const float *w, int32_t b,
+                        const float *X, const float *R, float gamma, float *Y,
+                        int32_t nthreads) {
+  if (b < 0 || (b > 0 && (!X || !R || !Y))) return ORA_EINVAL;
+  int rc = check_ids(n_e, n_r, n_t, subj, rel, obj);
+  if (rc) return rc;
+  int err = 0;
+#pragma omp parallel num_threads(pick_threads(nthreads, b))
+  {
+    double *acc = (double *)malloc(sizeof(double) * (size_t)(n_e > 0 ? n_e : 1));
+    if (!acc) {
+#pragma omp atomic write
+      err = 1;
+    }
+#pragma omp for schedule(dynamic, 1)
+    for (int32_t beta = 0; beta < b; ++beta) {
+      if (!acc) continue;
+      const float *x = X + (size_t)beta * n_e;
+      const float *r = R + (size_t)beta * n_r;
+      for (int64_t j = 0; j < n_e; ++j) acc[j] = 0.0;
+      for (int64_t l = 0; l < n_t; ++l)
+        acc[obj[l]] += weight_of(w, l) * (double)x[subj[l]] * (double)r[rel[l]];
+      float *y = Y + (size_t)beta * n_e;
+      for (int64_t j = 0; j < n_e; ++j) y[j] = (float)(acc[j] + (double)gamma * (double)x[j]);
+    }
+    free(acc);
+  }
+  return err ? ORA_ENOMEM : ORA_OK;
+}
+
+int ora_follow_backward_residual(int64_t n_e, int64_t n_r, int64_t n_t, const int32_t *subj,
+                                 const int32_t *rel, const int32_t *obj, const float *w,
+                                 int32_t b, const float *X, const float *R, const float *dY,
+                                 float gamma, float *dX, float *dR, int32_t nthreads) {
+  int rc = ora_follow_backward(n_e, n_r, n_t, subj, rel, obj, w, b, X, R, dY, NULL, dR, nthreads);
+  if (rc || !dX) return rc;
+  if (!R) return ORA_EINVAL;
+  int err = 0;
+#pragma omp parallel num_threads(pick_threads(nthreads, b))
+  {
+    double *ax = (double *)malloc(sizeof(double) * (size_t)(n_e > 0 ? n_e : 1));
+    if (!ax) {
+#pragma omp atomic write
+      err = 1;
+    }
+#pragma omp for schedule(dynamic, 1)
+    for (int32_t beta = 0; beta < b; ++beta) {
+      if (!ax) continue;
+      const float *dy = dY + (size_t)beta * n_e;
+      const float *r = R + (size_t)beta * n_r;
+      for (int64_t i = 0; i < n_e; ++i) ax[i] = 0.0;
+      for (int64_t l = 0; l < n_t; ++l)
+        ax[subj[l]] += weight_of(w, l) * (double)dy[obj[l]] * (double)r[rel[l]];
+      float *dx = dX + (size_t)beta * n_e;
+      for (int64_t i = 0; i < n_e; ++i) dx[i] = (float)(ax[i] + (double)gamma * (double)dy[i]);
+    }
+    free(ax);
+  }
+  return err ? ORA_ENOMEM : ORA_OK;
+}

@@ -396,3 +396,62 @@ def test_chain_gradients_finite_differences():
         fd = (chain.chain_loss(kb, n_e, n_r, x0, rho + h * U, tgt)
               - chain.chain_loss(kb, n_e, n_r, x0, rho - h * U, tgt)) / (2 * h)
         assert abs(fd - (drho[t] * U[t]).sum()) <= 1e-6 * max(1e-3, abs(fd))
+
+
+# ---------------------------------------------------------------------------
+# Residual hop and residual chains (Sec. 3.2 KB completion, App. E)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("gamma", [0.0, 1.0, -0.75])
+def test_residual_hop_against_dense(gamma):
+    n_e, n_r, b = 36, 5, 6
+    s, r, o, w = tiny_kb(121, n_e, n_r, 280, weighted=True)
+    X, R, dY = rand_inputs(121, b, n_e, n_r, signed=True)
+    Y = oracle.follow_residual(s, r, o, n_e, n_r, X, R, gamma, weight=w)
+    assert_rounded_once(Y, dense_ref.reified(s, r, o, n_e, n_r, X, R, w) + gamma * X.astype(np.float64))
+    dX, dR = oracle.follow_backward_residual(s, r, o, n_e, n_r, X, R, dY, gamma, weight=w)
+    dX_ref, dR_ref = dense_ref.reified_grads(s, r, o, n_e, n_r, X, R, dY, w)
+    assert_rounded_once(dX, dX_ref + gamma * dY.astype(np.float64))
+    assert_rounded_once(dR, dR_ref)
+    if gamma == 0.0:
+        assert np.array_equal(Y, oracle.follow(s, r, o, n_e, n_r, X, R, weight=w))
+
+
+def test_residual_chain_is_the_path_expansion():
+    # App. E: with x^t = f^t(x^{t-1}) + x^{t-1}, x^T expands by linearity into
+    # the sum, over every subset S of {1..T}, of the hops in S applied in order.
+    n_e, n_r, b, T = 30, 4, 3, 3
+    s, r, o, w = tiny_kb(131, n_e, n_r, 220, weighted=True)
+    g = np.random.default_rng(131)
+    x0 = g.random((b, n_e))
+    rs = [g.random((b, n_r)) for _ in range(T)]
+    xs = chain.residual_chain((s, r, o), n_e, n_r, x0, rs, weight=w)
+    total = np.zeros((b, n_e))
+    for mask in range(1 << T):
+        x = x0
+        for t in range(T):
+            if mask >> t & 1:
+                x = dense_ref.reified(s, r, o, n_e, n_r, x, rs[t], w)
+        total += x
+    np.testing.assert_allclose(xs[-1], total, rtol=1e-12, atol=1e-12)
+
+
+def test_residual_chain_gradients_finite_differences():
+    n_e, n_r, b, T = 25, 4, 2, 3
+    s, r, o, w = tiny_kb(141, n_e, n_r, 200, weighted=True)
+    g = np.random.default_rng(141)
+    x0 = g.standard_normal((b, n_e))
+    rs = [g.standard_normal((b, n_r)) for _ in range(T)]
+    G = g.standard_normal((b, n_e))
+    L = lambda x, rr: float((G * chain.residual_chain((s, r, o), n_e, n_r, x, rr, weight=w)[-1]).sum())
+    dx0, drs = chain.residual_chain_grad((s, r, o), n_e, n_r, x0, rs, G, weight=w)
+    h = 1e-3
+    V = g.standard_normal((b, n_e))
+    fd = (L(x0 + h * V, rs) - L(x0 - h * V, rs)) / (2 * h)   # exact: L is linear in x0
+    assert abs(fd - (dx0 * V).sum()) <= 1e-9 * max(1.0, abs(fd))
+    for t in range(T):
+        U = g.standard_normal((b, n_r))
+        plus = [rr + h * U if i == t else rr for i, rr in enumerate(rs)]
+        minus = [rr - h * U if i == t else rr for i, rr in enumerate(rs)]
+        fd = (L(x0, plus) - L(x0, minus)) / (2 * h)           # exact: L is linear in each r^t
+        assert abs(fd - (drs[t] * U).sum()) <= 1e-9 * max(1.0, abs(fd))
