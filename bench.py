@@ -96,6 +96,41 @@ def cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads):
     }
 
 
+def grid_sweep(args, torch, kbgen, kbf):
+    """Relation sweep of the grid scalability experiment (Sec. 3.1): the 2-hop
+    inference follow(follow(x, r), r) for minibatches of 128 one-hot queries,
+    reported as queries per second, for each relation count."""
+    n, b = args.grid, 128
+    torch.cuda.set_device(0)
+    rows = []
+    for m in [int(v) for v in args.grid_relations.split(",")]:
+        s, r, o = kbgen.grid_kb(n, m)
+        x, rr = kbgen.grid_inputs(n, m, b)
+        kb = kbf.KB(s, r, o, n * n, m)
+        X = torch.from_numpy(x).cuda().t().contiguous()
+        R = torch.from_numpy(rr).cuda().t().contiguous()
+        Y1, Y2 = torch.empty_like(X), torch.empty_like(X)
+        for _ in range(args.warmup):
+            kb.follow(kb.follow(X, R, out=Y1), R, out=Y2)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(args.steps):
+            kb.follow(kb.follow(X, R, out=Y1), R, out=Y2)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        rows.append({"relations": m, "triples": int(len(s)), "ms_per_minibatch": round(ms, 4),
+                     "qps": round(b / (ms * 1e-3), 1)})
+        log(f"[grid] n={n} m={m} {ms:.4f} ms per 2-hop minibatch, {b / (ms * 1e-3):.3e} qps")
+        kb.close()
+    print(json.dumps({"metric": "queries/s of 2-hop follow on an n x n grid KB", "unit": "qps",
+                      "higher_is_better": True, "n_gpus": 1, "data": "synthetic",
+                      "config": {"workload": "grid", "n": n, "entities": n * n, "batch": b},
+                      "sweep": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +143,14 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the HIP-event phase timing")
+    ap.add_argument("--residual", type=float, default=None, metavar="GAMMA",
+                    help="time the residual hop follow(X, R) + GAMMA * X and its backward "
+                         "(KB-completion chains) instead of the plain follow")
+    ap.add_argument("--grid", type=int, default=0, metavar="N",
+                    help="instead: queries/s of the 2-hop follow(follow(x, r), r) on the N x N "
+                         "grid KB of the scalability experiment (b = 128 one-hot queries)")
+    ap.add_argument("--grid-relations", default="4,20,100,1000",
+                    help="relation counts of the grid sweep (comma separated)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (to scale rocprofv3 "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -130,6 +173,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration": {"bytes_read": 4 * n, "bytes_written": 4 * n,
                                                "launches": 5}}))
+        return
+
+    if args.grid:
+        grid_sweep(args, torch, kbgen, kbf)
         return
 
     w = kbgen.WORKLOADS[args.workload]
@@ -155,8 +202,8 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step():
-        gkb.follow(X, R, out=Y, stream=stream)
-        gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream)
+        gkb.follow(X, R, out=Y, stream=stream, residual=args.residual)
+        gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream, residual=args.residual)
 
     for _ in range(args.warmup):
         step()
@@ -186,7 +233,7 @@ def main():
         ms_avg = phases[dom][0] / max(1, phases[dom][1])
         gather_b, comp_b = pass_bytes(kb, b, dom)
         sec = ms_avg * 1e-3
-        traffic = measured_traffic(w.name, b, dom)
+        traffic = measured_traffic(w.name, b, dom) if args.residual is None else None
         roof = {"bound": "hbm", "achieved": round(comp_b / sec / 1e9, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(comp_b / sec / 1e9 / PEAK_HBM_GBPS, 4),
                 "traffic": traffic,
@@ -224,7 +271,8 @@ def main():
         "config": {"workload": w.name, "n_entities": w.n_entities, "n_relations": w.n_relations,
                    "n_triples": kb.n_triples, "batch": b,
                    "laws": {"subj": w.subj_law, "obj": w.obj_law, "rel": w.rel_law},
-                   "x": w.x_kind, "r": w.r_kind, "dy": w.dy_kind, "parallelism": "single GPU"},
+                   "x": w.x_kind, "r": w.r_kind, "dy": w.dy_kind, "parallelism": "single GPU",
+                   "op": "follow" if args.residual is None else f"follow + {args.residual} * X"},
         "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
         "kb_create_s": round(create_s, 2),
         "roofline": roof,

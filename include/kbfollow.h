@@ -133,6 +133,25 @@ kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const fl
                              const float *dY, float *dX, float *dR, void *workspace,
                              size_t ws_bytes, void *stream);
 
+/*
+ * Residual hop of the KB-completion chains (Sec. 3.2, App. E), which add each
+ * hop's input back:  Y = follow(X, R) + gamma * X  (gamma = 1 in the paper).
+ * Arguments, layout and rules as for kb_follow; each element of Y is the
+ * double-precision sum plus gamma * X, rounded to float once.
+ */
+kb_status kb_follow_residual(const kb_t *kb, int32_t b, const float *X, const float *R,
+                             float gamma, float *Y, void *workspace, size_t ws_bytes,
+                             void *stream);
+
+/*
+ * Backward of kb_follow_residual for upstream gradient dY:
+ *   dX = (dX of kb_follow_backward) + gamma * dY,   dR as in kb_follow_backward.
+ * Arguments and rules as for kb_follow_backward.
+ */
+kb_status kb_follow_backward_residual(const kb_t *kb, int32_t b, const float *X, const float *R,
+                                      const float *dY, float gamma, float *dX, float *dR,
+                                      void *workspace, size_t ws_bytes, void *stream);
+
 /* Static description of a status code. */
 const char *kb_status_str(kb_status s);
 

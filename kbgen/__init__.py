@@ -372,3 +372,43 @@ def make_chain_inputs(w: Workload, kb: KB, hops: int = 3, sub: int = 0):
         k = int(gt.integers(1, 6))
         tgt[beta, gt.choice(n, size=k, replace=False)] = 1.0 / k
     return x0, rho, tgt
+
+
+# ----------------------------------------------------------------------------
+# grid KB of the scalability experiment (Sec. 3.1)
+# ----------------------------------------------------------------------------
+
+GRID_INDEX = 5      # seed slot of the grid workloads
+
+
+def grid_kb(n: int, n_relations: int = 4):
+    """The n x n grid KB: every cell is an entity linked to its neighbours by
+    north / south / east / west edges.  With n_relations = 4 the relation is
+    the direction; otherwise every edge gets one of n_relations invented
+    relation names uniformly at random (seeded), as in the relation sweep of
+    Sec. 3.1.  Cell (a, c) is entity a * n + c.  Returns int32 (subj, rel, obj)."""
+    a, c = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    a, c = a.ravel(), c.ravel()
+    subj, rel, obj = [], [], []
+    for k, (da, dc) in enumerate(((-1, 0), (1, 0), (0, 1), (0, -1))):
+        ok = (a + da >= 0) & (a + da < n) & (c + dc >= 0) & (c + dc < n)
+        subj.append(a[ok] * n + c[ok])
+        obj.append((a[ok] + da) * n + c[ok] + dc)
+        rel.append(np.full(int(ok.sum()), k))
+    subj, rel, obj = (np.concatenate(v).astype(np.int32) for v in (subj, rel, obj))
+    if n_relations != 4:
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+            [ROOT_SEED, GRID_INDEX, ST_TRIPLES, n, n_relations])))
+        rel = g.integers(0, n_relations, len(subj)).astype(np.int32)
+    return subj, rel, obj
+
+
+def grid_inputs(n: int, n_relations: int, batch: int = 128):
+    """One-hot random cells and relation weights 1 + U(0, 0.001) (the grid
+    experiments of App. E), in batch-major [b][N] orientation."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+        [ROOT_SEED, GRID_INDEX, ST_X, n, n_relations, batch])))
+    x = np.zeros((batch, n * n), np.float32)
+    x[np.arange(batch), g.integers(0, n * n, batch)] = 1.0
+    r = (1.0 + 0.001 * g.random((batch, n_relations))).astype(np.float32)
+    return x, r

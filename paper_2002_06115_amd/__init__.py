@@ -9,6 +9,7 @@ and the current stream.
     Y  = kb.follow(X, R)                                    # X [N_E][b], R [N_R][b]
     dX, dR = kb.follow_backward(X, R, dY)
     Y  = follow(kb, X, R)                                   # autograd-aware
+    Y  = follow_residual(kb, X, R)                          # follow(X, R) + X (App. E)
 
 Activations are entity-major and batch-contiguous float32 CUDA tensors:
 ``X[i, beta]`` is the weight of entity i in example beta (the transpose of the
@@ -68,6 +69,11 @@ def _load_library():
     lib.kb_follow.restype = ctypes.c_int
     lib.kb_follow_backward.argtypes = [p, i32, p, p, p, p, p, p, sz, p]
     lib.kb_follow_backward.restype = ctypes.c_int
+    f32 = ctypes.c_float
+    lib.kb_follow_residual.argtypes = [p, i32, p, p, f32, p, p, sz, p]
+    lib.kb_follow_residual.restype = ctypes.c_int
+    lib.kb_follow_backward_residual.argtypes = [p, i32, p, p, p, f32, p, p, p, sz, p]
+    lib.kb_follow_backward_residual.restype = ctypes.c_int
     lib.kb_status_str.argtypes = [ctypes.c_int]
     lib.kb_status_str.restype = ctypes.c_char_p
     lib.kb_last_error.argtypes = []
@@ -187,8 +193,12 @@ class KB:
         return None if t is None else ctypes.c_void_p(t.data_ptr())
 
     # -- the operations --------------------------------------------------------
-    def follow(self, X, R, out=None, stream=None):
-        """Y = follow(X, R) (Eq. 4) for X [N_E][b], R [N_R][b]; returns Y [N_E][b]."""
+    def follow(self, X, R, out=None, stream=None, residual=None):
+        """Y = follow(X, R) (Eq. 4) for X [N_E][b], R [N_R][b]; returns Y [N_E][b].
+
+        With ``residual=gamma``: Y = follow(X, R) + gamma * X, the hop of the
+        KB-completion chains (Sec. 3.2, App. E).
+        """
         import torch
         X = self._act(X, self.n_entities, "X")
         R = self._act(R, self.n_relations, "R")
@@ -198,15 +208,26 @@ class KB:
         Y = torch.empty_like(X) if out is None else self._act(out, self.n_entities, "out")
         ws = self.workspace(b)
         s = torch.cuda.current_stream(self.device) if stream is None else stream
+        nws = 0 if ws is None else ws.numel()
         with torch.cuda.device(self.device):
-            _check(_lib.kb_follow(self._handle, b, self._ptr(X), self._ptr(R), self._ptr(Y),
-                                  self._ptr(ws), 0 if ws is None else ws.numel(),
-                                  ctypes.c_void_p(s.cuda_stream)), "kb_follow")
+            if residual is None:
+                _check(_lib.kb_follow(self._handle, b, self._ptr(X), self._ptr(R), self._ptr(Y),
+                                      self._ptr(ws), nws, ctypes.c_void_p(s.cuda_stream)),
+                       "kb_follow")
+            else:
+                _check(_lib.kb_follow_residual(self._handle, b, self._ptr(X), self._ptr(R),
+                                               float(residual), self._ptr(Y), self._ptr(ws), nws,
+                                               ctypes.c_void_p(s.cuda_stream)),
+                       "kb_follow_residual")
         return Y
 
     def follow_backward(self, X, R, dY, want_dx=True, want_dr=True, dX=None, dR=None,
-                        stream=None):
-        """(dX [N_E][b], dR [N_R][b]) for upstream gradient dY [N_E][b]."""
+                        stream=None, residual=None):
+        """(dX [N_E][b], dR [N_R][b]) for upstream gradient dY [N_E][b].
+
+        With ``residual=gamma`` the gradients of follow(X, R) + gamma * X
+        (dX gains gamma * dY).
+        """
         import torch
         dY = self._act(dY, self.n_entities, "dY")
         b = dY.shape[1]
@@ -220,12 +241,18 @@ class KB:
         dR = self._act(dR, self.n_relations, "dR") if want_dr else None
         ws = self.workspace(b)
         s = torch.cuda.current_stream(self.device) if stream is None else stream
+        nws = 0 if ws is None else ws.numel()
         with torch.cuda.device(self.device):
-            _check(_lib.kb_follow_backward(self._handle, b, self._ptr(X), self._ptr(R),
-                                           self._ptr(dY), self._ptr(dX), self._ptr(dR),
-                                           self._ptr(ws), 0 if ws is None else ws.numel(),
-                                           ctypes.c_void_p(s.cuda_stream)),
-                   "kb_follow_backward")
+            if residual is None:
+                _check(_lib.kb_follow_backward(self._handle, b, self._ptr(X), self._ptr(R),
+                                               self._ptr(dY), self._ptr(dX), self._ptr(dR),
+                                               self._ptr(ws), nws, ctypes.c_void_p(s.cuda_stream)),
+                       "kb_follow_backward")
+            else:
+                _check(_lib.kb_follow_backward_residual(
+                    self._handle, b, self._ptr(X), self._ptr(R), self._ptr(dY), float(residual),
+                    self._ptr(dX), self._ptr(dR), self._ptr(ws), nws,
+                    ctypes.c_void_p(s.cuda_stream)), "kb_follow_backward_residual")
         return dX, dR
 
     # -- event timing -----------------------------------------------------------
@@ -241,23 +268,24 @@ class KB:
         return {p: (ms[i], n[i]) for i, p in enumerate(PHASES)}
 
 
-def _make_function():
+def _make_functions():
     import torch
 
     class _Follow(torch.autograd.Function):
         @staticmethod
-        def forward(ctx, X, R, kb):
+        def forward(ctx, X, R, kb, residual):
             ctx.kb = kb
+            ctx.residual = residual
             ctx.save_for_backward(X, R)
-            return kb.follow(X, R)
+            return kb.follow(X, R, residual=residual)
 
         @staticmethod
         def backward(ctx, dY):
             X, R = ctx.saved_tensors
             need_x, need_r = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
             dX, dR = ctx.kb.follow_backward(X, R, dY.contiguous(), want_dx=need_x,
-                                            want_dr=need_r)
-            return dX, dR, None
+                                            want_dr=need_r, residual=ctx.residual)
+            return dX, dR, None, None
 
     return _Follow
 
@@ -269,8 +297,16 @@ def follow(kb: KB, X, R):
     """Differentiable follow(X, R) (Eq. 4) on entity-major tensors X [N_E][b], R [N_R][b]."""
     global _FollowFn
     if _FollowFn is None:
-        _FollowFn = _make_function()
-    return _FollowFn.apply(X, R, kb)
+        _FollowFn = _make_functions()
+    return _FollowFn.apply(X, R, kb, None)
 
 
-__all__ = ["KB", "KBError", "follow", "layout_host", "LIB_PATH", "PHASES"]
+def follow_residual(kb: KB, X, R, gamma: float = 1.0):
+    """Differentiable residual hop follow(X, R) + gamma * X (Sec. 3.2, App. E)."""
+    global _FollowFn
+    if _FollowFn is None:
+        _FollowFn = _make_functions()
+    return _FollowFn.apply(X, R, kb, float(gamma))
+
+
+__all__ = ["KB", "KBError", "follow", "follow_residual", "layout_host", "LIB_PATH", "PHASES"]

@@ -186,14 +186,18 @@ kb_status check_device(const kb_t *kb) {
   return KB_OK;
 }
 
-// Runs one pass: the stream kernel, the combine levels, the empty rows.
+// Runs one pass: the stream kernel, the combine levels, the empty rows.  With
+// residual set (A has one row per output row) every output row j also gets
+// gamma * A[j].
 kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float *A,
                    int64_t A_rows, const float *B, int64_t B_rows, int32_t b, float *out,
-                   void *ws, hipStream_t s) {
+                   void *ws, bool residual, float gamma, hipStream_t s) {
   double *slots = static_cast<double *>(ws);
+  const float *res = residual ? A : nullptr;
   {
     PhaseScope scope(kb, ph_base + 0, s);
-    StreamArgs a{D.entries, D.weights, D.n, D.chunk, A, A_rows, B, B_rows, b, out, slots};
+    StreamArgs a{D.entries, D.weights, D.n, D.chunk, A, A_rows, B, B_rows, b, out, slots,
+                 residual ? 1 : 0, gamma};
     hipError_t e = launch_stream(a, kb->plain_loads, s);
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
@@ -201,13 +205,13 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
     PhaseScope scope(kb, ph_base + 1, s);
     for (size_t L = 0; L + 1 < D.level_begin.size(); ++L) {
       const int64_t n = D.level_begin[L + 1] - D.level_begin[L];
-      hipError_t e = launch_combine(D.ctasks + D.level_begin[L], n, slots, b, out, s);
+      hipError_t e = launch_combine(D.ctasks + D.level_begin[L], n, slots, b, out, res, gamma, s);
       if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
     }
   }
   {
     PhaseScope scope(kb, ph_base + 2, s);
-    hipError_t e = launch_zero_rows(D.empty, D.n_empty, b, out, s);
+    hipError_t e = launch_zero_rows(D.empty, D.n_empty, b, out, res, gamma, s);
     if (e != hipSuccess) return hip_fail(e, "zero-rows kernel launch");
   }
   return KB_OK;
@@ -374,8 +378,12 @@ kb_status kb_get_info(const kb_t *kb, kb_info_t *info) {
   return KB_OK;
 }
 
-kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, float *Y,
-                    void *workspace, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+kb_status follow_impl(const kb_t *kb, int32_t b, const float *X, const float *R, bool residual,
+                      float gamma, float *Y, void *workspace, size_t ws_bytes, void *stream) {
   try {
     if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
     if (b < 1) return fail(KB_EINVAL, "b must be >= 1");
@@ -395,15 +403,15 @@ kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, f
     if (!ent_bytes) return KB_OK;
     // By object, runs of equal relation: Y[o] = sum over runs of R[r] (.) sum of X[s].
     return run_pass(kb, kb->L[BY_OBJ], KB_PH_FWD_STREAM, X, kb->n_entities, R, kb->n_relations,
-                    b, Y, workspace, static_cast<hipStream_t>(stream));
+                    b, Y, workspace, residual, gamma, static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(KB_EINVAL, "unexpected host error");
   }
 }
 
-kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const float *R,
-                             const float *dY, float *dX, float *dR, void *workspace,
-                             size_t ws_bytes, void *stream) {
+kb_status backward_impl(const kb_t *kb, int32_t b, const float *X, const float *R,
+                        const float *dY, bool residual, float gamma, float *dX, float *dR,
+                        void *workspace, size_t ws_bytes, void *stream) {
   try {
     if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
     if (b < 1) return fail(KB_EINVAL, "b must be >= 1");
@@ -431,21 +439,49 @@ kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const fl
     g_last_error.clear();
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (want_dx) {
-      // By subject, runs of equal relation: dX[s] = sum over runs of R[r] (.) sum of dY[o].
+      // By subject, runs of equal relation: dX[s] = sum over runs of R[r] (.) sum of dY[o]
+      // (+ gamma * dY[s] for the residual hop).
       st = run_pass(kb, kb->L[BY_SUBJ], KB_PH_DX_STREAM, dY, kb->n_entities, R, kb->n_relations,
-                    b, dX, workspace, s);
+                    b, dX, workspace, residual, gamma, s);
       if (st != KB_OK) return st;
     }
     if (want_dr) {
       // By relation, runs of equal subject: dR[k] = sum over runs of X[s] (.) sum of dY[o].
       st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_STREAM, dY, kb->n_entities, X, kb->n_entities,
-                    b, dR, workspace, s);
+                    b, dR, workspace, false, 0.0f, s);
       if (st != KB_OK) return st;
     }
     return KB_OK;
   } catch (...) {
     return fail(KB_EINVAL, "unexpected host error");
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, float *Y,
+                    void *workspace, size_t ws_bytes, void *stream) {
+  return follow_impl(kb, b, X, R, false, 0.0f, Y, workspace, ws_bytes, stream);
+}
+
+kb_status kb_follow_residual(const kb_t *kb, int32_t b, const float *X, const float *R,
+                             float gamma, float *Y, void *workspace, size_t ws_bytes,
+                             void *stream) {
+  return follow_impl(kb, b, X, R, true, gamma, Y, workspace, ws_bytes, stream);
+}
+
+kb_status kb_follow_backward_residual(const kb_t *kb, int32_t b, const float *X, const float *R,
+                                      const float *dY, float gamma, float *dX, float *dR,
+                                      void *workspace, size_t ws_bytes, void *stream) {
+  return backward_impl(kb, b, X, R, dY, true, gamma, dX, dR, workspace, ws_bytes, stream);
+}
+
+kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const float *R,
+                             const float *dY, float *dX, float *dR, void *workspace,
+                             size_t ws_bytes, void *stream) {
+  return backward_impl(kb, b, X, R, dY, false, 0.0f, dX, dR, workspace, ws_bytes, stream);
 }
 
 kb_status kb_profile_enable(kb_t *kb, int32_t on) {

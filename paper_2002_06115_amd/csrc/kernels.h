@@ -27,7 +27,10 @@ constexpr int32_t kChunkQuantum = 8;
 //     run += w[p] * A[a]                      for every triple
 //     acc += run (.) B[b_id], run = 0         at a triple flagged run-end
 //     target = acc (float row / double slot), acc = 0   at a marker
-// A has A_rows rows and B has B_rows rows of b floats.
+// A has A_rows rows and B has B_rows rows of b floats.  With `residual` set
+// (A then has one row per output row), a marker writing row j writes
+// acc + gamma * A[j] instead: the residual hop follow(X, R) + gamma * X of the
+// KB-completion chains, and its dX pass (A = dY there).
 struct StreamArgs {
   const int2 *entries;
   const float *weights;  // per entry, nullptr for a hard KB
@@ -40,17 +43,21 @@ struct StreamArgs {
   int32_t b;
   float *out;
   double *slots;
+  int32_t residual;
+  float gamma;
 };
 // plain_loads forces the plain-load variant (used anyway for tables of 4 GB
 // or more) so it can be tested at small sizes.
 hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s);
 
-// Sums workspace slots in order (one combine level).
+// Sums workspace slots in order (one combine level).  A final row write adds
+// gamma * res[row] when res is not null (residual hop).
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int32_t b,
-                          float *out, hipStream_t s);
+                          float *out, const float *res, float gamma, hipStream_t s);
 
-// Writes +0.0 to the listed rows of out ([rows][b]).
+// Writes +0.0 to the listed rows of out ([rows][b]), or gamma * res[row] when
+// res is not null (residual hop).
 hipError_t launch_zero_rows(const int32_t *rows, int64_t n_rows, int32_t b, float *out,
-                            hipStream_t s);
+                            const float *res, float gamma, hipStream_t s);
 
 }  // namespace kbf

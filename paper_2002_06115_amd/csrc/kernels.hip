@@ -152,7 +152,7 @@ __device__ __forceinline__ void store_slot(double *__restrict__ p, const double 
 // ends): such a lane returns zeros and generates no memory traffic, and no
 // load sits behind a branch.  Without BUF, plain loads read row 0 of A at
 // markers and every triple's B row.
-template <int VEC, int LPT, bool BUF, bool WEIGHTED>
+template <int VEC, int LPT, bool BUF, bool WEIGHTED, bool RES>
 __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   constexpr int GPB = kBlock / LPT;
   const int lane = threadIdx.x % LPT;
@@ -216,9 +216,13 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
       for (int u = 0; u < kUnroll; ++u) {
         const bool triple = e[u].x >= 0;
         const bool run_end = triple && (e[u].x & kRunEnd);
-        const size_t ia = triple ? (size_t)(e[u].x & kIdMask) : 0;
+        // A marker that writes row j of a residual pass reads A[j] for gamma * A[j].
+        const bool res_row = RES && !triple && e[u].y >= 0;
+        const size_t ia = triple ? (size_t)(e[u].x & kIdMask) : (res_row ? (size_t)e[u].y : 0);
         if constexpr (BUF) {
-          load_row_buffer<VEC>(arsrc, triple ? (uint32_t)((ia * bb + cl) * sizeof(float)) : kOutOfRange,
+          load_row_buffer<VEC>(arsrc,
+                               (triple || res_row) ? (uint32_t)((ia * bb + cl) * sizeof(float))
+                                                   : kOutOfRange,
                                xa[u]);
           load_row_buffer<VEC>(brsrc,
                                run_end ? (uint32_t)(((size_t)e[u].y * bb + cl) * sizeof(float))
@@ -242,18 +246,27 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
         for (int v = 0; v < VEC; ++v) {
           double t = (double)xa[u][v];
           if constexpr (WEIGHTED) t *= (double)w[u];
-          // (Buffer loads already return exact zeros at markers.)
-          run[v] += (BUF || triple) ? t : 0.0;
+          // (Buffer loads already return exact zeros at markers, except the
+          // residual row of a residual pass.)
+          run[v] += ((BUF && !RES) || triple) ? t : 0.0;
           const double closed = acc[v] + run[v] * (double)xb[u][v];
           acc[v] = run_end ? closed : acc[v];
           run[v] = run_end ? 0.0 : run[v];
         }
         const int f = e[u].y;
         if (!triple && active && f != INT_MIN) {
-          if (f >= 0)
-            store_row<VEC>(a.out + (size_t)f * bb + c, acc);
-          else
+          if (f >= 0) {
+            if constexpr (RES) {
+              double y[VEC];
+#pragma unroll
+              for (int v = 0; v < VEC; ++v) y[v] = acc[v] + (double)a.gamma * (double)xa[u][v];
+              store_row<VEC>(a.out + (size_t)f * bb + c, y);
+            } else {
+              store_row<VEC>(a.out + (size_t)f * bb + c, acc);
+            }
+          } else {
             store_slot<VEC>(a.slots + (size_t)(-(f + 1)) * bb + c, acc);
+          }
         }
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[v] = triple ? acc[v] : 0.0;
@@ -268,7 +281,9 @@ template <int VEC, int LPT>
 __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict__ tasks,
                                                          int64_t n_tasks,
                                                          double *__restrict__ slots, int32_t b,
-                                                         float *__restrict__ out) {
+                                                         float *__restrict__ out,
+                                                         const float *__restrict__ res,
+                                                         float gamma) {
   constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
   const int lane = threadIdx.x % LPT;
@@ -295,52 +310,75 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
           for (int v = 0; v < VEC; ++v) acc[v] += part[u][v];
         }
     }
-    if (tk.z >= 0)
+    if (tk.z >= 0) {
+      if (res) {
+        float r[VEC];
+        load_row<VEC>(res + (size_t)tk.z * bb + c, r);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[v] += (double)gamma * (double)r[v];
+      }
       store_row<VEC>(out + (size_t)tk.z * bb + c, acc);
-    else
+    } else {
       store_slot<VEC>(slots + (size_t)(-(tk.z + 1)) * bb + c, acc);
+    }
   }
 }
 
 template <int VEC>
 __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__restrict__ rows,
                                                            int64_t n_rows, int32_t b,
-                                                           float *__restrict__ out) {
+                                                           float *__restrict__ out,
+                                                           const float *__restrict__ res,
+                                                           float gamma) {
   const int per_row = b / VEC;
   const int64_t total = n_rows * per_row;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
     const int64_t q = e / per_row;
     const int j = (int)(e - q * per_row);
-    float *p = out + (size_t)rows[q] * (size_t)b + (size_t)j * VEC;
+    const size_t off = (size_t)rows[q] * (size_t)b + (size_t)j * VEC;
+    double y[VEC];
+    if (res) {
+      float r[VEC];
+      load_row<VEC>(res + off, r);
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) y[v] = 0.0 + (double)gamma * (double)r[v];
+    } else {
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) y[v] = 0.0;
+    }
     if constexpr (VEC == 4)
-      *reinterpret_cast<float4 *>(p) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      *reinterpret_cast<float4 *>(out + off) =
+          make_float4((float)y[0], (float)y[1], (float)y[2], (float)y[3]);
     else
-      *p = 0.0f;
+      out[off] = (float)y[0];
   }
 }
 
-template <int VEC, bool BUF, bool WT>
+template <int VEC, bool BUF, bool WT, bool RES>
 const void *stream_fn(int lpt) {
   switch (lpt) {
-    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, BUF, WT>);
-    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, BUF, WT>);
-    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, BUF, WT>);
-    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, BUF, WT>);
-    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, BUF, WT>);
-    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, BUF, WT>);
-    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, BUF, WT>);
+    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, BUF, WT, RES>);
+    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, BUF, WT, RES>);
+    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, BUF, WT, RES>);
+    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, BUF, WT, RES>);
+    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, BUF, WT, RES>);
+    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, BUF, WT, RES>);
+    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, BUF, WT, RES>);
   }
   return nullptr;
 }
 
-const void *stream_fn_for(const ColumnTiling &t, bool buf, bool wt) {
-  if (t.vec == 4) {
-    if (buf) return wt ? stream_fn<4, true, true>(t.lpt) : stream_fn<4, true, false>(t.lpt);
-    return wt ? stream_fn<4, false, true>(t.lpt) : stream_fn<4, false, false>(t.lpt);
-  }
-  if (buf) return wt ? stream_fn<1, true, true>(t.lpt) : stream_fn<1, true, false>(t.lpt);
-  return wt ? stream_fn<1, false, true>(t.lpt) : stream_fn<1, false, false>(t.lpt);
+template <int VEC, bool BUF>
+const void *stream_fn_buf(int lpt, bool wt, bool res) {
+  if (wt) return res ? stream_fn<VEC, BUF, true, true>(lpt) : stream_fn<VEC, BUF, true, false>(lpt);
+  return res ? stream_fn<VEC, BUF, false, true>(lpt) : stream_fn<VEC, BUF, false, false>(lpt);
+}
+
+const void *stream_fn_for(const ColumnTiling &t, bool buf, bool wt, bool res) {
+  if (t.vec == 4)
+    return buf ? stream_fn_buf<4, true>(t.lpt, wt, res) : stream_fn_buf<4, false>(t.lpt, wt, res);
+  return buf ? stream_fn_buf<1, true>(t.lpt, wt, res) : stream_fn_buf<1, false>(t.lpt, wt, res);
 }
 
 template <int VEC>
@@ -385,7 +423,7 @@ hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
   const uint64_t row_bytes = (uint64_t)a.b * sizeof(float);
   const bool buf = !plain_loads && (uint64_t)a.A_rows * row_bytes <= (uint64_t)kOutOfRange &&
                    (uint64_t)a.B_rows * row_bytes <= (uint64_t)kOutOfRange;
-  const void *fn = stream_fn_for(t, buf, a.weights != nullptr);
+  const void *fn = stream_fn_for(t, buf, a.weights != nullptr, a.residual != 0);
   if (!fn) return hipErrorInvalidValue;
   if (a.chunk % kChunkQuantum != 0 || a.n % a.chunk != 0) return hipErrorInvalidValue;
   const int64_t n_chunks = a.n / a.chunk;
@@ -396,26 +434,28 @@ hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
 }
 
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int32_t b,
-                          float *out, hipStream_t s) {
+                          float *out, const float *res, float gamma, hipStream_t s) {
   if (n_tasks == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(b);
   const void *fn = t.vec == 4 ? combine_fn<4>(t.lpt) : combine_fn<1>(t.lpt);
   if (!fn) return hipErrorInvalidValue;
   const dim3 grid((unsigned)blocks_for(n_tasks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
-  void *params[] = {&tasks, &n_tasks, &slots, &b, &out};
+  void *params[] = {&tasks, &n_tasks, &slots, &b, &out, &res, &gamma};
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 
 hipError_t launch_zero_rows(const int32_t *rows, int64_t n_rows, int32_t b, float *out,
-                            hipStream_t s) {
+                            const float *res, float gamma, hipStream_t s) {
   if (n_rows == 0) return hipSuccess;
   const int vec = (b % 4 == 0) ? 4 : 1;
   const int64_t items = n_rows * (b / vec);
   const dim3 grid((unsigned)blocks_for(items, kBlock, 256 * 64));
   if (vec == 4)
-    hipLaunchKernelGGL(zero_rows_kernel<4>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out);
+    hipLaunchKernelGGL(zero_rows_kernel<4>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, res,
+                       gamma);
   else
-    hipLaunchKernelGGL(zero_rows_kernel<1>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out);
+    hipLaunchKernelGGL(zero_rows_kernel<1>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, res,
+                       gamma);
   return hipGetLastError();
 }
 

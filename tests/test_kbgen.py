@@ -64,3 +64,15 @@ def test_chain_seeds_reach_three_hops():
     assert x0.shape == (256, 1000) and np.all(x0.sum(axis=1) == 1)
     assert rho.shape == (3, 256, 10)
     np.testing.assert_allclose(tgt.sum(axis=1), 1.0, rtol=1e-6)
+
+
+def test_grid_kb_shape():
+    s, r, o = kbgen.grid_kb(5)
+    assert len(s) == 4 * 5 * 4            # 2 n (n - 1) edges per axis, both directions
+    assert set(r.tolist()) == {0, 1, 2, 3}
+    for ss, oo in zip(s.tolist(), o.tolist()):
+        assert abs(ss // 5 - oo // 5) + abs(ss % 5 - oo % 5) == 1
+    s2, r2, o2 = kbgen.grid_kb(5, 50)
+    assert np.array_equal(s, s2) and np.array_equal(o, o2) and r2.max() < 50
+    x, rr = kbgen.grid_inputs(5, 50, 16)
+    assert np.all(x.sum(axis=1) == 1) and np.all((rr >= 1.0) & (rr <= 1.001))
