@@ -56,21 +56,40 @@ def pass_bytes(kb, b, phase):
     return float(gather), float(comp)
 
 
-def measured_traffic(workload, b, phase):
+def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False):
+    """Mangled name of the stream-kernel instance a pass launches for batch b:
+    VEC = 4 floats per lane when b % 4 == 0 (else 1), LPT = lanes per group
+    (b / VEC rounded up to a power of two, at most 64), raw-buffer loads unless
+    a table reaches 4 GB."""
+    vec = 4 if b % 4 == 0 else 1
+    lanes, lpt = -(-b // vec), 1
+    while lpt < lanes and lpt < 64:
+        lpt *= 2
+    flag = lambda v: 1 if v else 0
+    return (f"_ZN3kbf12_GLOBAL__N_113stream_kernelILi{vec}ELi{lpt}ELb{flag(not plain_loads)}"
+            f"ELb{flag(weighted)}ELb{flag(residual)}EEEvNS_10StreamArgsE")
+
+
+def measured_traffic(workload, b, phase, symbol):
     """DRAM bytes of one launch from the committed rocprofv3 counters, if they
-    were taken on the device code that is built now (same fingerprint)."""
+    were taken on the device code of the kernel that is built now (same
+    per-kernel assembly digest)."""
     import glob
     fp_path = os.path.join(ROOT, "paper_2002_06115_amd", "_lib", "kernels.fingerprint")
-    if not os.path.exists(fp_path):
+    try:
+        digest = json.load(open(fp_path)).get(symbol)
+    except (OSError, ValueError):
         return None
-    fp = open(fp_path).read().strip()
+    if not digest:
+        return None
     for path in glob.glob(os.path.join(ROOT, "profiles", "*.json")):
         try:
             prof = json.load(open(path))
         except (OSError, ValueError):
             continue
         if prof.get("workload") == workload and prof.get("batch") == b \
-                and prof.get("fingerprint") == fp and phase in prof.get("per_launch", {}):
+                and prof.get("symbol") == symbol and prof.get("kernel_sha") == digest \
+                and phase in prof.get("per_launch", {}):
             return float(prof["per_launch"][phase]["bytes"])
     return None
 
@@ -233,7 +252,9 @@ def main():
         ms_avg = phases[dom][0] / max(1, phases[dom][1])
         gather_b, comp_b = pass_bytes(kb, b, dom)
         sec = ms_avg * 1e-3
-        traffic = measured_traffic(w.name, b, dom) if args.residual is None else None
+        symbol = stream_kernel_symbol(b, residual=args.residual is not None,
+                                      plain_loads=os.environ.get("KBFOLLOW_PLAIN_LOADS") == "1")
+        traffic = measured_traffic(w.name, b, dom, symbol)
         roof = {"bound": "hbm", "achieved": round(comp_b / sec / 1e9, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(comp_b / sec / 1e9 / PEAK_HBM_GBPS, 4),
                 "traffic": traffic,

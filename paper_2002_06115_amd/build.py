@@ -68,23 +68,34 @@ def build(verbose: bool = False, defines=(), out=None, build_dir=None, src_dir=N
     return out
 
 
-def fingerprint(defines, path, bdir, csrc=CSRC) -> str:
-    """sha256 of the gfx950 assembly of kernels.hip (compiler-unique ids
-    removed): identifies the device code that rocprofv3 counters were taken on."""
+def fingerprint(defines, path, bdir, csrc=CSRC) -> dict:
+    """Per-kernel sha256 of the gfx950 assembly of kernels.hip, written as JSON
+    {mangled kernel name: digest}: identifies the device code that rocprofv3
+    counters were taken on (compiler-unique ids and debug lines excluded)."""
     import hashlib
+    import json
+    import re
     asm = os.path.join(bdir, "kernels.s")
     cmd = [hipcc(), "-x", "hip", "--cuda-device-only", "-S", *DEVICE_FLAGS, *COMMON_FLAGS,
            "-I", csrc, *[f"-D{d}" for d in defines], os.path.join(csrc, "kernels.hip"), "-o", asm]
     subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
-    h = hashlib.sha256()
+    digests, name, h = {}, None, None
+    start = re.compile(r"^(_Z\S+):\s*(;.*)?$")
     with open(asm) as f:
         for line in f:
-            if "__hip_cuid" not in line and not line.lstrip().startswith((".file", ".ident")):
-                h.update(line.encode())
-    digest = h.hexdigest()
+            m = start.match(line)
+            if m and name is None:
+                name, h = m.group(1), hashlib.sha256()
+                continue
+            if name is not None:
+                if line.startswith(".Lfunc_end"):
+                    digests[name] = h.hexdigest()
+                    name = None
+                elif "__hip_cuid" not in line and not line.lstrip().startswith((".loc", ".file")):
+                    h.update(line.encode())
     with open(path, "w") as f:
-        f.write(digest + "\n")
-    return digest
+        json.dump(digests, f, indent=0, sort_keys=True)
+    return digests
 
 
 if __name__ == "__main__":
