@@ -196,8 +196,8 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
   const float *res = residual ? A : nullptr;
   {
     PhaseScope scope(kb, ph_base + 0, s);
-    StreamArgs a{D.entries, D.weights, D.n, D.chunk, A, A_rows, B, B_rows, b, out, slots,
-                 residual ? 1 : 0, gamma};
+    StreamArgs a{D.entries, D.weights, D.n, D.chunk, A, A_rows, B, B_rows, b, out, D.rows,
+                 slots, D.n_slots, residual ? 1 : 0, gamma};
     hipError_t e = launch_stream(a, kb->plain_loads, s);
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }

@@ -20,12 +20,12 @@ ColumnTiling column_tiling(int32_t b);
 constexpr int32_t kChunkQuantum = 8;
 
 // Segmented gather-multiply-sum over one layout's entry stream (every pass
-// of the library).  entries[p] = (x, y): a triple x = a | run-end flag,
+// of the library).  entries[p] = (x, y): a triple x = a | run-start flag,
 // y = b_id, or a marker x = -1, y = target (row, -(slot + 1), or INT32_MIN
 // for none); n is a multiple of chunk, and chunk of kChunkQuantum.  Lane
 // group g walks entries [g * chunk, (g + 1) * chunk):
-//     run += w[p] * A[a]                      for every triple
-//     acc += run (.) B[b_id], run = 0         at a triple flagged run-end
+//     held = B[b_id]                          at a triple flagged run-start
+//     acc += w[p] * A[a] (.) held             for every triple
 //     target = acc (float row / double slot), acc = 0   at a marker
 // A has A_rows rows and B has B_rows rows of b floats.  With `residual` set
 // (A then has one row per output row), a marker writing row j writes
@@ -42,7 +42,9 @@ struct StreamArgs {
   int64_t B_rows;
   int32_t b;
   float *out;
+  int64_t out_rows;
   double *slots;
+  int64_t n_slots;
   int32_t residual;
   float gamma;
 };

@@ -138,20 +138,55 @@ __device__ __forceinline__ void store_slot(double *__restrict__ p, const double 
   }
 }
 
+template <int VEC>
+__device__ __forceinline__ void store_slot_buffer(__amdgpu_buffer_rsrc_t rsrc, uint32_t off,
+                                                  const double (&acc)[VEC]) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+  if constexpr (VEC == 4) {
+    const double2 lo = make_double2(acc[0], acc[1]), hi = make_double2(acc[2], acc[3]);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, lo), rsrc, (int)off, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, hi), rsrc, (int)(off + 16), 0,
+                                           0);
+  } else {
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, acc[0]), rsrc, (int)off, 0, 0);
+  }
+}
+
+// Stores of VEC floats / doubles at byte offset `off` of a raw buffer; rows
+// written once per pass use the non-temporal policy.
+constexpr int kNonTemporal = 2;
+template <int VEC>
+__device__ __forceinline__ void store_row_buffer(__amdgpu_buffer_rsrc_t rsrc, uint32_t off,
+                                                 const double (&y)[VEC]) {
+  if constexpr (VEC == 4) {
+    const native_float4 v = {(float)y[0], (float)y[1], (float)y[2], (float)y[3]};
+    __builtin_amdgcn_raw_buffer_store_b128(
+        __builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned int, v), rsrc, (int)off, 0,
+        kNonTemporal);
+  } else {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint((float)y[0]), rsrc, (int)off, 0,
+                                          kNonTemporal);
+  }
+}
+
 // One lane group (LPT lanes) per chunk of the entry stream; chunks are
 // visited grid-stride so a capped (persistent) grid works too.  Every chunk
 // holds the same number of entries, so the work is balanced whatever the row
 // lengths.
 //
-// Inside a row the triples come in runs of equal B id.  The group sums the A
-// rows of a run (in double) and multiplies the sum by the B row once, at the
-// run's last triple: B is read once per run, not once per triple.
+// Inside a row the triples come in runs of equal B id.  The group reads the
+// B row once, at the run's first triple, keeps it in registers for the run,
+// and adds w * A[a] * B[b_id] for every triple with one double FMA per
+// column (the product of two floats is exact in double).
 //
-// With BUF (A and B each under 4 GB) both are read with raw buffer loads whose
-// offset is out of range where no row is needed (A at markers, B except at run
-// ends): such a lane returns zeros and generates no memory traffic, and no
-// load sits behind a branch.  Without BUF, plain loads read row 0 of A at
-// markers and every triple's B row.
+// With BUF (A, B, the output and the workspace each under 4 GB) all reads are
+// raw buffer loads with 32-bit offsets; where no row is needed (A at markers,
+// B except at run starts) the offset is out of range, so the lane gets zeros
+// and generates no memory traffic, and no load sits behind a branch.  A
+// marker therefore finds A = 0 and a held B row of 0, so its FMA adds an
+// exact zero.  Without BUF, plain loads read row 0 at markers and the values
+// are masked instead.
 template <int VEC, int LPT, bool BUF, bool WEIGHTED, bool RES>
 __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   constexpr int GPB = kBlock / LPT;
@@ -162,14 +197,19 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   const size_t bb = (size_t)a.b;
   // Lanes past b read column 0 and store nothing.
   const int cl = active ? c : 0;
+  const uint32_t row_bytes = (uint32_t)a.b * (uint32_t)sizeof(float);
+  const uint32_t col_bytes = (uint32_t)cl * (uint32_t)sizeof(float);
 
-  // (Only used with BUF, where A and B are known to be under 4 GB.)
-  const __amdgpu_buffer_rsrc_t arsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float *>(a.A), 0, (int)(uint32_t)(a.A_rows * a.b * sizeof(float)),
-      kRawBufferWord3);
-  const __amdgpu_buffer_rsrc_t brsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float *>(a.B), 0, (int)(uint32_t)(a.B_rows * a.b * sizeof(float)),
-      kRawBufferWord3);
+  // (Only used with BUF, where every table is known to be under 4 GB.)
+  auto rsrc = [](const void *p, uint64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, (int)(uint32_t)bytes,
+                                             kRawBufferWord3);
+  };
+  const __amdgpu_buffer_rsrc_t arsrc = rsrc(a.A, (uint64_t)a.A_rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t brsrc = rsrc(a.B, (uint64_t)a.B_rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t orsrc = rsrc(a.out, (uint64_t)a.out_rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t srsrc =
+      rsrc(a.slots, (uint64_t)a.n_slots * a.b * sizeof(double));
 
   const int64_t n_chunks = a.n / a.chunk;
   const int64_t stride = (int64_t)gridDim.x * GPB;
@@ -192,9 +232,13 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
   for (int64_t g = (int64_t)blockIdx.x * GPB + grp; g < n_chunks; g += stride) {
     const int64_t p0 = g * a.chunk;
     const int64_t p1 = p0 + a.chunk;
-    double acc[VEC], run[VEC];
+    double acc[VEC];
+    float held_b[VEC];  // the current run's B row
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) acc[v] = run[v] = 0.0;
+    for (int v = 0; v < VEC; ++v) {
+      acc[v] = 0.0;
+      held_b[v] = 0.0f;
+    }
 
     // Software pipeline: the entries of the next step are loaded while this
     // step's gathers are in flight.
@@ -215,57 +259,57 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const bool triple = e[u].x >= 0;
-        const bool run_end = triple && (e[u].x & kRunEnd);
+        const bool run_start = triple && (e[u].x & kRunStart);
         // A marker that writes row j of a residual pass reads A[j] for gamma * A[j].
         const bool res_row = RES && !triple && e[u].y >= 0;
-        const size_t ia = triple ? (size_t)(e[u].x & kIdMask) : (res_row ? (size_t)e[u].y : 0);
+        const uint32_t ia = triple ? (uint32_t)(e[u].x & kIdMask) : (uint32_t)e[u].y;
         if constexpr (BUF) {
-          load_row_buffer<VEC>(arsrc,
-                               (triple || res_row) ? (uint32_t)((ia * bb + cl) * sizeof(float))
-                                                   : kOutOfRange,
+          load_row_buffer<VEC>(arsrc, (triple || res_row) ? ia * row_bytes + col_bytes : kOutOfRange,
                                xa[u]);
-          load_row_buffer<VEC>(brsrc,
-                               run_end ? (uint32_t)(((size_t)e[u].y * bb + cl) * sizeof(float))
-                                       : kOutOfRange,
+          load_row_buffer<VEC>(brsrc, run_start ? (uint32_t)e[u].y * row_bytes + col_bytes
+                                                : kOutOfRange,
                                xb[u]);
         } else {
-          load_row<VEC>(a.A + ia * bb + cl, xa[u]);
-          load_row<VEC>(a.B + (size_t)(triple ? e[u].y : 0) * bb + cl, xb[u]);
+          load_row<VEC>(a.A + (size_t)(triple || res_row ? ia : 0) * bb + cl, xa[u]);
+          load_row<VEC>(a.B + (size_t)(run_start ? e[u].y : 0) * bb + cl, xb[u]);
         }
       }
       fetch(p + kUnroll, mine_next, wmine_next);
-      // Branch-free accumulation: selects, not branches, decide what an entry
-      // does (a select also keeps an Inf or NaN row from leaking into a sum it
-      // does not belong to, as a multiply by zero would); only the store of a
-      // marker is predicated.
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const bool triple = e[u].x >= 0;
-        const bool run_end = triple && (e[u].x & kRunEnd);
+        const bool run_start = triple && (e[u].x & kRunStart);
+        // Run starts take the new B row; markers take the zeros their
+        // out-of-range B load returned (masked explicitly without BUF).
+        const bool take_b = run_start || !triple;
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
+          const float nb = (BUF || triple) ? xb[u][v] : 0.0f;
+          held_b[v] = take_b ? nb : held_b[v];
           double t = (double)xa[u][v];
           if constexpr (WEIGHTED) t *= (double)w[u];
-          // (Buffer loads already return exact zeros at markers, except the
-          // residual row of a residual pass.)
-          run[v] += ((BUF && !RES) || triple) ? t : 0.0;
-          const double closed = acc[v] + run[v] * (double)xb[u][v];
-          acc[v] = run_end ? closed : acc[v];
-          run[v] = run_end ? 0.0 : run[v];
+          // Zero at markers (also the residual row's A and plain loads' row 0).
+          if constexpr (RES || !BUF) t = triple ? t : 0.0;
+          acc[v] = __builtin_fma(t, (double)held_b[v], acc[v]);
         }
         const int f = e[u].y;
         if (!triple && active && f != INT_MIN) {
-          if (f >= 0) {
-            if constexpr (RES) {
-              double y[VEC];
+          double y[VEC];
 #pragma unroll
-              for (int v = 0; v < VEC; ++v) y[v] = acc[v] + (double)a.gamma * (double)xa[u][v];
+          for (int v = 0; v < VEC; ++v)
+            y[v] = (RES && f >= 0) ? acc[v] + (double)a.gamma * (double)xa[u][v] : acc[v];
+          if (f >= 0) {
+            if constexpr (BUF)
+              store_row_buffer<VEC>(orsrc, (uint32_t)f * row_bytes + col_bytes, y);
+            else
               store_row<VEC>(a.out + (size_t)f * bb + c, y);
-            } else {
-              store_row<VEC>(a.out + (size_t)f * bb + c, acc);
-            }
           } else {
-            store_slot<VEC>(a.slots + (size_t)(-(f + 1)) * bb + c, acc);
+            if constexpr (BUF)
+              store_slot_buffer<VEC>(srsrc, ((uint32_t)(-(f + 1)) * (uint32_t)a.b + (uint32_t)c) *
+                                                (uint32_t)sizeof(double),
+                                     y);
+            else
+              store_slot<VEC>(a.slots + (size_t)(-(f + 1)) * bb + c, y);
           }
         }
 #pragma unroll
@@ -421,8 +465,10 @@ hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
   const ColumnTiling t = column_tiling(a.b);
   // Raw-buffer offsets are 32-bit: tables of 4 GB or more take plain loads.
   const uint64_t row_bytes = (uint64_t)a.b * sizeof(float);
-  const bool buf = !plain_loads && (uint64_t)a.A_rows * row_bytes <= (uint64_t)kOutOfRange &&
-                   (uint64_t)a.B_rows * row_bytes <= (uint64_t)kOutOfRange;
+  const uint64_t lim = kOutOfRange;
+  const bool buf = !plain_loads && (uint64_t)a.A_rows * row_bytes <= lim &&
+                   (uint64_t)a.B_rows * row_bytes <= lim && (uint64_t)a.out_rows * row_bytes <= lim &&
+                   (uint64_t)a.n_slots * (uint64_t)a.b * sizeof(double) <= lim;
   const void *fn = stream_fn_for(t, buf, a.weights != nullptr, a.residual != 0);
   if (!fn) return hipErrorInvalidValue;
   if (a.chunk % kChunkQuantum != 0 || a.n % a.chunk != 0) return hipErrorInvalidValue;

@@ -129,7 +129,6 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
       if ((int64_t)S.size() % chunk == chunk - 1) {
         // The chunk's last entry must be a marker.
         if (pending) {
-          S.back().x |= kRunEnd;  // fold the open run before the partial is written
           if (n_slots == 0) first_slot = P.n_slots;
           marker(-(int32_t)P.n_slots - 1);
           ++P.n_slots;
@@ -139,8 +138,9 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
         }
         pending = false;
       }
-      const bool run_end = p + 1 == end || L.col_b[p + 1] != L.col_b[p];
-      S.push_back({L.col_a[p] | (run_end ? kRunEnd : 0), L.col_b[p]});
+      // A run starts after every marker and wherever col_b changes.
+      const bool run_start = !pending || L.col_b[p] != L.col_b[p - 1];
+      S.push_back({L.col_a[p] | (run_start ? kRunStart : 0), L.col_b[p]});
       if (weighted) P.weights.push_back(L.weight[p]);
       pending = true;
     }

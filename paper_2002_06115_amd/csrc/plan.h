@@ -36,15 +36,16 @@ struct LayoutHost {
 };
 
 // One 8-byte stream entry.  A triple: x = (id gathered for this triple, col_a)
-// | kRunEnd when it is the last triple of a run of equal col_b, y = col_b.  A
-// marker (x = kMarker): write the running sum to y -- a row (y >= 0), a
-// workspace slot -(y + 1), or nothing (y = kNoTarget) -- and restart from zero.
+// | kRunStart when it is the first triple of a run of equal col_b since the
+// last marker, y = col_b.  A marker (x = kMarker): write the running sum to y
+// -- a row (y >= 0), a workspace slot -(y + 1), or nothing (y = kNoTarget) --
+// and restart from zero.
 struct Entry {
   int32_t x, y;
 };
 constexpr int32_t kMarker = -1;
-constexpr int32_t kRunEnd = 1 << 30;
-constexpr int32_t kIdMask = kRunEnd - 1;
+constexpr int32_t kRunStart = 1 << 30;
+constexpr int32_t kIdMask = kRunStart - 1;
 constexpr int32_t kNoTarget = INT32_MIN;
 
 // The stream plan of one layout.  The sorted triples of every non-empty row
@@ -56,8 +57,8 @@ constexpr int32_t kNoTarget = INT32_MIN;
 // marker writes its last partial to a slot too.  A row's slots are numbered
 // consecutively in chunk order and summed in that order by combine tasks, at
 // most `fan_in` slots per task, over as many levels as the row needs.
-// Inside a row the triples form runs of equal col_b; the kernel multiplies a
-// run's summed A rows by its B row once, at the entry flagged kRunEnd.
+// Inside a row the triples form runs of equal col_b; the kernel reads a run's
+// B row once, at the entry flagged kRunStart, and keeps it for the run.
 struct PlanHost {
   int32_t chunk = 0;
   int32_t fan_in = 0;
