@@ -104,6 +104,11 @@ def cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads):
     oracle.follow(s, r, o, n_e, n_r, Xs, Rs, nthreads=threads)
     oracle.follow_backward(s, r, o, n_e, n_r, Xs, Rs, dYs, nthreads=threads)
     dt = time.perf_counter() - t0
+    # One thread on one batch column: the per-core rate.
+    t0 = time.perf_counter()
+    oracle.follow(s, r, o, n_e, n_r, Xs[:1], Rs[:1], nthreads=1)
+    oracle.follow_backward(s, r, o, n_e, n_r, Xs[:1], Rs[:1], dYs[:1], nthreads=1)
+    dt1 = time.perf_counter() - t0
     return {
         "value": kb.n_triples * cols / dt,
         "unit": "triple·batch/s",
@@ -111,8 +116,144 @@ def cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads):
         "kind": "oracle",
         "sample": (f"same KB, {cols} of {X_bm.shape[0]} batch columns, forward + dX + dR, "
                    f"{dt:.1f} s on {min(threads, cols)} threads of {os.cpu_count()} "
-                   f"({platform.processor() or platform.machine()})"),
+                   f"({cpu_model()})"),
+        "single_thread_value": kb.n_triples / dt1,
+        "single_thread_sample": f"1 batch column on 1 thread, forward + dX + dR, {dt1:.1f} s",
     }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def percentiles(v):
+    q = np.percentile(np.asarray(v, dtype=np.float64), [10, 50, 90])
+    return {"p10": round(float(q[0]), 4), "p50": round(float(q[1]), 4), "p90": round(float(q[2]), 4)}
+
+
+def timing_detail(torch, fwd, bwd, stream, iters, flush=None):
+    """Per-iteration HIP-event times of the forward and the backward (ms),
+    as p10 / median / p90.  With `flush` (a 1 GiB device buffer, larger than
+    the 256 MB last-level cache) the buffer is overwritten before every
+    iteration, so each one starts with cold caches."""
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(iters)]
+    for i in range(iters):
+        if flush is not None:
+            flush.fill_(float(i))
+        ev[i][0].record(stream)
+        fwd()
+        ev[i][1].record(stream)
+        bwd()
+        ev[i][2].record(stream)
+    torch.cuda.synchronize()
+    f = [e[0].elapsed_time(e[1]) for e in ev]
+    g = [e[1].elapsed_time(e[2]) for e in ev]
+    return {"iters": iters, "fwd_ms": percentiles(f), "bwd_ms": percentiles(g),
+            "fwd_bwd_ms": percentiles([a + c for a, c in zip(f, g)])}
+
+
+def copy_bandwidth(torch, reps=10):
+    """Read + write GB/s of a plain 1 GiB device-to-device copy."""
+    n = (1 << 30) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    del src, dst
+    return round(2 * 4 * n / (ms * 1e-3) / 1e9, 1)
+
+
+def gather_probe(args, torch, kbgen, kbf):
+    """The memory system's own rate for each pass's row reads: a pure gather
+    (libkbprobe.so, no products, no second operand, no output rows) of the
+    index stream a pass reads per triple, beside the pass's stream-kernel
+    time, plus uniformly random indices for reference."""
+    import ctypes
+    from paper_2002_06115_amd import build as kbuild
+    if not os.path.exists(kbuild.PROBE_LIB):
+        raise SystemExit(f"{kbuild.PROBE_LIB} is not built (run __graft_entry__.build())")
+    lib = ctypes.CDLL(kbuild.PROBE_LIB)
+    lib.kbp_gather_time.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                    ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                    ctypes.c_int32, ctypes.c_void_p,
+                                    ctypes.POINTER(ctypes.c_float)]
+    w = kbgen.WORKLOADS[args.workload]
+    kb = kbgen.make_kb(w)
+    torch.cuda.set_device(0)
+    em = lambda a: torch.from_numpy(a).cuda().t().contiguous()
+    X, R, dY = em(kbgen.make_x(w)), em(kbgen.make_r(w)), em(kbgen.make_dy(w))
+    b, chunk = w.batch, 256
+    gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
+    Y, dX, dR = torch.empty_like(X), torch.empty_like(X), torch.empty_like(R)
+    gkb.follow(X, R, out=Y)
+    gkb.follow_backward(X, R, dY, dX=dX, dR=dR)
+    torch.cuda.synchronize()
+    gkb.profile(True)
+    for _ in range(args.steps):
+        gkb.follow(X, R, out=Y)
+        gkb.follow_backward(X, R, dY, dX=dX, dR=dR)
+    ph = gkb.profile_read()
+    gkb.profile(False)
+    passes = {k: round(ph[k][0] / max(1, ph[k][1]), 4) for k in ("fwd_stream", "dx_stream",
+                                                                  "dr_stream")}
+    lib.kbp_stream_read_time.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                         ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.POINTER(ctypes.c_float)]
+    big = torch.ones((2 << 30) // 4, device="cuda")
+    reads = []
+    for blocks in (1024, 4096, 16384):
+        scratch = torch.empty(blocks * 256, device="cuda")
+        ms = ctypes.c_float()
+        if lib.kbp_stream_read_time(big.data_ptr(), big.numel() // 4, blocks, scratch.data_ptr(),
+                                    10, ctypes.c_void_p(None), ctypes.byref(ms)) != 0:
+            raise SystemExit("kbp_stream_read_time failed")
+        reads.append(round(big.numel() * 4 / (ms.value * 1e-3) / 1e9, 1))
+    del big, scratch
+    stream_read = max(reads)
+    log(f"[probe] sequential read of 2 GiB: {reads} GB/s")
+    lay = {which: kbf.layout_host(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations, which)
+           for which in (0, 1, 2)}
+    rng = np.random.default_rng(np.random.SeedSequence([20020615, 99]))
+    streams = [
+        ("forward: subjects in object order, rows of X", lay[0][1], X),
+        ("dX: objects in subject order, rows of dY", lay[1][1], dY),
+        ("dR: objects in relation order, rows of dY", lay[2][1], dY),
+        ("dR: subjects in relation order, rows of X", lay[2][2], X),
+        ("uniform random entity ids, rows of X",
+         rng.integers(0, w.n_entities, kb.n_triples).astype(np.int32), X),
+    ]
+    rows = []
+    for name, ids, table in streams:
+        idx = torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).cuda()
+        n = idx.numel()
+        out = torch.empty(((n + chunk - 1) // chunk) * b, device="cuda")
+        ms = ctypes.c_float()
+        rc = lib.kbp_gather_time(idx.data_ptr(), n, chunk, table.data_ptr(), b, out.data_ptr(),
+                                 max(1, args.steps), ctypes.c_void_p(None), ctypes.byref(ms))
+        if rc != 0:
+            raise SystemExit(f"kbp_gather_time failed ({rc})")
+        rows.append({"stream": name, "rows": n, "ms": round(ms.value, 4),
+                     "gathered_GBps": round(n * 4 * b / (ms.value * 1e-3) / 1e9, 1)})
+        log(f"[probe] {name}: {ms.value:.4f} ms")
+        del idx, out
+    print(json.dumps({"metric": "pure-gather time of each pass's per-triple row reads",
+                      "config": {"workload": w.name, "batch": b, "chunk": chunk},
+                      "stream_kernel_ms": passes, "sequential_read_GBps": stream_read,
+                      "probe": rows}), flush=True)
+    gkb.close()
 
 
 def grid_sweep(args, torch, kbgen, kbf):
@@ -170,6 +311,12 @@ def main():
                          "grid KB of the scalability experiment (b = 128 one-hot queries)")
     ap.add_argument("--grid-relations", default="4,20,100,1000",
                     help="relation counts of the grid sweep (comma separated)")
+    ap.add_argument("--detail-iters", type=int, default=-1,
+                    help="iterations of the per-pass timing with percentiles, warm and cold "
+                         "cache (-1: 50 for the large KBs, 200 for metaqa, 1000 for tiny; 0: skip)")
+    ap.add_argument("--gather-probe", action="store_true",
+                    help="instead: time a pure gather of each pass's per-triple row reads "
+                         "(the memory system's rate for that access pattern) beside the passes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (to scale rocprofv3 "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -196,6 +343,9 @@ def main():
 
     if args.grid:
         grid_sweep(args, torch, kbgen, kbf)
+        return
+    if args.gather_probe:
+        gather_probe(args, torch, kbgen, kbf)
         return
 
     w = kbgen.WORKLOADS[args.workload]
@@ -246,6 +396,21 @@ def main():
     value = kb.n_triples * b / (ms_step * 1e-3)
     log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.3e} triple*batch/s")
 
+    detail = None
+    iters = args.detail_iters
+    if iters < 0:
+        iters = {"tiny": 1000, "metaqa": 200}.get(w.name, 50)
+    if iters > 0:
+        fwd = lambda: gkb.follow(X, R, out=Y, stream=stream, residual=args.residual)
+        bwd = lambda: gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream,
+                                          residual=args.residual)
+        detail = {"warm": timing_detail(torch, fwd, bwd, stream, iters)}
+        flush = torch.empty((1 << 30) // 4, device="cuda")
+        detail["cold"] = timing_detail(torch, fwd, bwd, stream, iters, flush=flush)
+        del flush
+        detail["copy_GBps"] = copy_bandwidth(torch)
+        log(f"[bench] detail {json.dumps(detail)}")
+
     roof = None
     if phases:
         dom = max(("fwd_stream", "dx_stream", "dr_stream"), key=lambda p: phases[p][0])
@@ -267,6 +432,12 @@ def main():
         if traffic:
             roof["hbm_measured_GBps"] = round(traffic / sec / 1e9, 1)
             roof["hbm_measured_frac"] = round(traffic / sec / 1e9 / PEAK_HBM_GBPS, 4)
+        if detail:
+            copy = detail["copy_GBps"]
+            roof["copy_GBps"] = copy
+            roof["achieved_frac_of_copy"] = round(comp_b / sec / 1e9 / copy, 4)
+            if traffic:
+                roof["hbm_measured_frac_of_copy"] = round(traffic / sec / 1e9 / copy, 4)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -296,6 +467,7 @@ def main():
                    "op": "follow" if args.residual is None else f"follow + {args.residual} * X"},
         "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
         "kb_create_s": round(create_s, 2),
+        "timing": detail,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
