@@ -391,11 +391,9 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__rest
 #pragma unroll
       for (int v = 0; v < VEC; ++v) y[v] = 0.0;
     }
-    if constexpr (VEC == 4)
-      *reinterpret_cast<float4 *>(out + off) =
-          make_float4((float)y[0], (float)y[1], (float)y[2], (float)y[3]);
-    else
-      out[off] = (float)y[0];
+    // Non-temporal, like every output row: plain stores would leave the
+    // rows dirty in the caches, to be written back during the next pass.
+    store_row<VEC>(out + off, y);
   }
 }
 

@@ -36,9 +36,9 @@ def sample_ids(ids_deg, k_random, rng, n):
 _KB_CACHE = {}
 
 
-def run_workload(kbf, w, integer):
+def run_workload(kbf, w, integer, weighted=False):
     import torch
-    print(f"[fullsize] generating {w.label} integer={integer}", flush=True)
+    print(f"[fullsize] generating {w.label} integer={integer} weighted={weighted}", flush=True)
     if w.name not in _KB_CACHE:
         _KB_CACHE.clear()
         _KB_CACHE[w.name] = kbgen.make_kb(w)
@@ -47,22 +47,32 @@ def run_workload(kbf, w, integer):
         X, R, dY = kbgen.make_integer_inputs(w)
     else:
         X, R, dY = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
+    # Soft-KB weights (App. A): one positive weight per triple.
+    wt = (np.random.default_rng(11).uniform(0.1, 2.0, kb.n_triples).astype(np.float32)
+          if weighted else None)
     print(f"[fullsize] kb_create {w.label}", flush=True)
-    gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
+    gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations, weight=wt)
     em = lambda a: torch.from_numpy(a).cuda().t().contiguous()
     Xe, Re, dYe = em(X), em(R), em(dY)
     Y = gkb.follow(Xe, Re)
     dX, dR = gkb.follow_backward(Xe, Re, dYe)
+    # A second call, in the launch configuration bench.py times, is bitwise equal.
+    Y2 = gkb.follow(Xe, Re)
+    dX2, dR2 = gkb.follow_backward(Xe, Re, dYe)
     torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int32)
+    for name, t1, t2 in (("Y", Y, Y2), ("dX", dX, dX2), ("dR", dR, dR2)):
+        assert torch.equal(bits(t1), bits(t2)), f"{w.name} {name} differs between two calls"
+    del Y2, dX2, dR2
     print(f"[fullsize] GPU pass done {w.label}", flush=True)
     rng = np.random.default_rng(7)
     objs = sample_ids(np.bincount(kb.obj, minlength=w.n_entities), 48, rng, w.n_entities)
     subs = sample_ids(np.bincount(kb.subj, minlength=w.n_entities), 48, rng, w.n_entities)
     rels = sample_ids(np.bincount(kb.rel, minlength=w.n_relations), 8, rng, w.n_relations)
     args = (kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
-    want_y = oracle.sampled(oracle.SAMPLE_Y, *args, objs, X=X, R=R)
-    want_dx = oracle.sampled(oracle.SAMPLE_DX, *args, subs, R=R, dY=dY)
-    want_dr = oracle.sampled(oracle.SAMPLE_DR, *args, rels, X=X, dY=dY)
+    want_y = oracle.sampled(oracle.SAMPLE_Y, *args, objs, X=X, R=R, weight=wt)
+    want_dx = oracle.sampled(oracle.SAMPLE_DX, *args, subs, R=R, dY=dY, weight=wt)
+    want_dr = oracle.sampled(oracle.SAMPLE_DR, *args, rels, X=X, dY=dY, weight=wt)
     idx = lambda t, ids: t[torch.from_numpy(ids.astype(np.int64)).cuda()].t().contiguous().cpu().numpy()
     got = (idx(Y, objs), idx(dX, subs), idx(dR, rels))
     check = assert_bitexact if integer else assert_close
@@ -81,6 +91,11 @@ def test_large_fullsize(kbf, integer):
     run_workload(kbf, kbgen.LARGE, integer)
 
 
+def test_large_fullsize_soft_kb(kbf):
+    run_workload(kbf, kbgen.LARGE, False, weighted=True)
+
+
 @pytest.mark.parametrize("integer", [True, False])
 def test_train_fullsize(kbf, integer):
     run_workload(kbf, kbgen.TRAIN, integer)
+

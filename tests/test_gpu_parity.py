@@ -91,14 +91,20 @@ def test_weighted_kb(kbf):
     check(kbf, w, kb, kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w), False, "weighted", weight=wt)
 
 
-def test_deterministic(kbf):
-    w = SCALED["large_s"]
+@pytest.mark.parametrize("name", list(SCALED))
+def test_deterministic(kbf, name):
+    """Two calls on the same inputs give bitwise-equal Y, dX and dR: no
+    atomics, every sum in a fixed order (also with a freshly built KB)."""
+    w = SCALED[name]
     kb = kbgen.make_kb(w)
     X, R, dY = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
-    a = run_gpu(kbf, (kb.subj, kb.rel, kb.obj), w.n_entities, w.n_relations, X, R, dY)
-    c = run_gpu(kbf, (kb.subj, kb.rel, kb.obj), w.n_entities, w.n_relations, X, R, dY, kb=a[3])
-    for g1, g2 in zip(a[:3], c[:3]):
+    arrays = (kb.subj, kb.rel, kb.obj)
+    a = run_gpu(kbf, arrays, w.n_entities, w.n_relations, X, R, dY)
+    c = run_gpu(kbf, arrays, w.n_entities, w.n_relations, X, R, dY, kb=a[3])
+    d = run_gpu(kbf, arrays, w.n_entities, w.n_relations, X, R, dY)
+    for g1, g2, g3 in zip(a[:3], c[:3], d[:3]):
         assert np.array_equal(g1.view(np.uint32), g2.view(np.uint32))
+        assert np.array_equal(g1.view(np.uint32), g3.view(np.uint32))
 
 
 def chain_gpu(kbf, kb, x0, rho, target):
@@ -145,6 +151,12 @@ def test_three_hop_chain(kbf):
     assert_close(dx0_g, dx0_o, "chain dx0")
     for t in range(3):
         assert_close(drho_g[t], drho_o[t], f"chain drho{t + 1}")
+    # The whole three-hop chain is bitwise reproducible.
+    loss_2, dx0_2, drho_2 = chain_gpu(kbf, gkb, x0, rho, tgt)
+    assert loss_2 == loss_g
+    assert np.array_equal(dx0_2, dx0_g)
+    for t in range(3):
+        assert np.array_equal(drho_2[t], drho_g[t])
 
 
 def test_autograd_function(kbf):
