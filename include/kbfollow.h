@@ -105,9 +105,10 @@ size_t kb_workspace_size(const kb_t *kb, int32_t b);
  *   R          : DEVICE float [N_R][b], read only.
  *   Y          : DEVICE float [N_E][b], fully overwritten; must not overlap X or R.
  *   workspace  : DEVICE scratch of at least kb_workspace_size(kb, b) bytes,
- *                256-byte aligned (may be NULL when that size is 0).  Its
- *                contents on entry are ignored.  Calls running at the same
- *                time must not share one.
+ *                256-byte aligned (may be NULL when that size is 0; at
+ *                least 16-byte alignment is enforced).  It must not overlap
+ *                X, R or Y.  Its contents on entry are ignored.  Calls
+ *                running at the same time must not share one.
  *   ws_bytes   : size of workspace in bytes.
  *   stream     : hipStream_t on which the work is enqueued.
  *
@@ -126,8 +127,9 @@ kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, f
  *              NULL when dR is NULL, R may be NULL when dX is NULL.
  *   dX       : DEVICE float [N_E][b], overwritten, or NULL to skip it.
  *   dR       : DEVICE float [N_R][b], overwritten, or NULL to skip it.
- *   Outputs must not overlap each other or any input.  Workspace and stream as
- *   for kb_follow (dX and dR reuse the same workspace one after the other).
+ *   Outputs must not overlap each other or any input, and the workspace
+ *   overlaps none of the arrays.  Workspace and stream as for kb_follow (dX
+ *   and dR reuse the same workspace one after the other).
  */
 kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const float *R,
                              const float *dY, float *dX, float *dR, void *workspace,

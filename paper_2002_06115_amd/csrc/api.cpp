@@ -6,8 +6,10 @@
 #include <climits>
 #include <cstdlib>
 #include <cstring>
+#include <initializer_list>
 #include <new>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "kbfollow.h"
@@ -159,12 +161,17 @@ struct PhaseScope {
     if (!kb->timing.on) return;
     start = take(kb->timing);
     stop = take(kb->timing);
-    if (start) (void)hipEventRecord(start, s);
+    if (start && stop) (void)hipEventRecord(start, s);
   }
   ~PhaseScope() {
-    if (!start || !stop) return;
-    (void)hipEventRecord(stop, s);
-    kb->timing.recs.push_back({phase, start, stop});
+    if (start && stop) {
+      (void)hipEventRecord(stop, s);
+      kb->timing.recs.push_back({phase, start, stop});
+      return;
+    }
+    // Only one event could be created: keep it for later, record nothing.
+    if (start) kb->timing.pool.push_back(start);
+    if (stop) kb->timing.pool.push_back(stop);
   }
 };
 
@@ -224,7 +231,10 @@ size_t workspace_bytes(const kb_t *kb, int32_t b) {
   return (bytes + 255) / 256 * 256;
 }
 
-kb_status check_ws(const kb_t *kb, int32_t b, void *ws, size_t ws_bytes) {
+// The workspace must be big enough, aligned, and clear of every array the
+// call reads or writes (arrays[i] of bytes[i]; null entries are skipped).
+kb_status check_ws(const kb_t *kb, int32_t b, void *ws, size_t ws_bytes,
+                   std::initializer_list<std::pair<const void *, size_t>> arrays) {
   const size_t need = workspace_bytes(kb, b);
   if (need == 0) return KB_OK;
   if (!ws) return fail(KB_EINVAL, "workspace is NULL but " + std::to_string(need) + " bytes are needed");
@@ -232,6 +242,9 @@ kb_status check_ws(const kb_t *kb, int32_t b, void *ws, size_t ws_bytes) {
     return fail(KB_EINVAL, "workspace has " + std::to_string(ws_bytes) + " bytes, " +
                                std::to_string(need) + " are needed");
   if (!aligned(ws, 16)) return fail(KB_EINVAL, "workspace must be 16-byte aligned");
+  for (const auto &a : arrays)
+    if (overlaps(ws, need, a.first, a.second))
+      return fail(KB_EINVAL, "workspace overlaps an input or output array");
   return KB_OK;
 }
 
@@ -396,7 +409,8 @@ kb_status follow_impl(const kb_t *kb, int32_t b, const float *X, const float *R,
       return fail(KB_EINVAL, "X, R and Y must be " + std::to_string(al) + "-byte aligned");
     if (overlaps(Y, ent_bytes, X, ent_bytes) || overlaps(Y, ent_bytes, R, rel_bytes))
       return fail(KB_EINVAL, "Y overlaps X or R");
-    kb_status st = check_ws(kb, b, workspace, ws_bytes);
+    kb_status st =
+        check_ws(kb, b, workspace, ws_bytes, {{X, ent_bytes}, {R, rel_bytes}, {Y, ent_bytes}});
     if (st != KB_OK) return st;
     if ((st = check_device(kb)) != KB_OK) return st;
     g_last_error.clear();
@@ -433,7 +447,9 @@ kb_status backward_impl(const kb_t *kb, int32_t b, const float *X, const float *
     if (want_dr && (overlaps(dR, rel_bytes, X, ent_bytes) || overlaps(dR, rel_bytes, R, rel_bytes) ||
                     overlaps(dR, rel_bytes, dY, ent_bytes)))
       return fail(KB_EINVAL, "dR overlaps another array");
-    kb_status st = check_ws(kb, b, workspace, ws_bytes);
+    kb_status st = check_ws(kb, b, workspace, ws_bytes,
+                            {{X, ent_bytes}, {R, rel_bytes}, {dY, ent_bytes},
+                             {want_dx ? dX : nullptr, ent_bytes}, {want_dr ? dR : nullptr, rel_bytes}});
     if (st != KB_OK) return st;
     if ((st = check_device(kb)) != KB_OK) return st;
     g_last_error.clear();

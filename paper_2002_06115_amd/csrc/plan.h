@@ -52,9 +52,10 @@ constexpr int32_t kNoTarget = INT32_MIN;
 // are followed by a marker that writes the row, and the stream is cut into
 // chunks of `chunk` entries, one chunk per lane group, whatever the row
 // lengths (Zipf hubs and one-triple rows alike); the stream is padded with
-// no-op markers to whole chunks.  The last entry of every chunk is a marker: where a row continues past it, that marker writes the
-// chunk's partial sum of the row to a workspace slot, and the row's final
-// marker writes its last partial to a slot too.  A row's slots are numbered
+// no-op markers to whole chunks.  The last entry of every chunk is a marker:
+// where a row continues past it, that marker writes the chunk's partial sum of
+// the row to a workspace slot, and the row's final marker writes its last
+// partial to a slot too.  A row's slots are numbered
 // consecutively in chunk order and summed in that order by combine tasks, at
 // most `fan_in` slots per task, over as many levels as the row needs.
 // Inside a row the triples form runs of equal col_b; the kernel reads a run's

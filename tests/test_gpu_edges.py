@@ -123,6 +123,20 @@ def test_argument_errors(kbf):
     Xo = torch.zeros(100 * 8 + 1, device="cuda")[1:].view(100, 8)
     Y = torch.zeros((100, 8), device="cuda")
     assert lib.kb_follow(h, 8, p(Xo), p(R), p(Y), wsp, nws, None) == kbf.KB_EINVAL      # misaligned
+    need = lib.kb_workspace_size(h, 8)
+    assert need > 0  # rows of this small KB cross its 16-entry chunks
+    # A workspace overlapping an input or an output is refused before any launch.
+    big = torch.zeros(need // 4 + 2 * 100 * 8, device="cuda")
+    inside = big[: 100 * 8].view(100, 8)
+    dX = torch.zeros((100, 8), device="cuda")
+    dR = torch.zeros((3, 8), device="cuda")
+    assert lib.kb_follow(h, 8, p(inside), p(R), p(Y), p(big), need, None) == kbf.KB_EINVAL
+    assert lib.kb_follow(h, 8, p(X), p(R), p(inside), p(big), need, None) == kbf.KB_EINVAL
+    assert lib.kb_follow_backward(h, 8, p(X), p(R), p(Y), p(inside), p(dR), p(big), need,
+                                  None) == kbf.KB_EINVAL
+    assert b"overlaps" in lib.kb_last_error()
+    assert lib.kb_follow_backward(h, 8, p(X), p(R), p(Y), p(dX), p(dR), wsp, nws,
+                                  None) == kbf.KB_OK
     torch.cuda.synchronize()
     with pytest.raises(ValueError):
         kb.follow(X, torch.zeros((3, 7), device="cuda"))
