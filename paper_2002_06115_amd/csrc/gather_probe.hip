@@ -6,7 +6,8 @@
 // time against this probe's time on the same index stream tells how far the
 // pass is from the memory system's own rate for that access pattern.
 //
-// A sequential read of a large buffer gives the streaming rate beside it.
+// A sequential read and a copy of a large buffer give the streaming rates
+// beside it.
 //
 // Same lane layout as the follow kernels: a lane group of LPT lanes reads one
 // row (lane l owns columns [4l, 4l + 4)) and walks one chunk of the index
@@ -79,6 +80,15 @@ __global__ __launch_bounds__(kBlock) void stream_read_kernel(const native_float4
   out[(int64_t)blockIdx.x * kBlock + threadIdx.x] = acc;
 }
 
+// Copy of n float4s, grid-stride, non-temporal stores.
+__global__ __launch_bounds__(kBlock) void stream_copy_kernel(const native_float4 *__restrict__ X,
+                                                             int64_t n,
+                                                             native_float4 *__restrict__ Y) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
+    __builtin_nontemporal_store(__builtin_nontemporal_load(X + i), Y + i);
+}
+
 // One untimed launch, then `reps` launches between two events on `s`;
 // *ms = mean time of one.  0 on success, -2 on a HIP error.
 template <class Run>
@@ -121,6 +131,22 @@ int kbp_stream_read_time(const void *X, int64_t n_float4, int32_t n_blocks, floa
   auto run = [&]() {
     hipLaunchKernelGGL(stream_read_kernel, dim3((unsigned)n_blocks), dim3(kBlock), 0, s,
                        static_cast<const native_float4 *>(X), n_float4, out);
+  };
+  return time_launches(run, reps, s, ms);
+}
+
+// Copies n_float4 float4s from DEVICE X to DEVICE Y (not overlapping), front
+// to back, `reps` timed launches after one untimed; *ms receives the mean
+// time of one.  n_blocks >= 1 workgroups of 256.  Returns 0, -1 for bad
+// arguments, -2 for a HIP error.
+int kbp_stream_copy_time(const void *X, void *Y, int64_t n_float4, int32_t n_blocks, int32_t reps,
+                         void *stream, float *ms) {
+  if (!X || !Y || !ms || n_float4 < 1 || n_blocks < 1 || reps < 1) return -1;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto run = [&]() {
+    hipLaunchKernelGGL(stream_copy_kernel, dim3((unsigned)n_blocks), dim3(kBlock), 0, s,
+                       static_cast<const native_float4 *>(X), n_float4,
+                       static_cast<native_float4 *>(Y));
   };
   return time_launches(run, reps, s, ms);
 }

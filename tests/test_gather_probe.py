@@ -30,6 +30,23 @@ def test_probe_library_exports_entry_points():
     lib = ctypes.CDLL(PROBE)
     assert hasattr(lib, "kbp_gather_time")
     assert hasattr(lib, "kbp_stream_read_time")
+    assert hasattr(lib, "kbp_stream_copy_time")
+
+
+def _copy_lib():
+    lib = ctypes.CDLL(PROBE)
+    lib.kbp_stream_copy_time.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.POINTER(ctypes.c_float)]
+    return lib
+
+
+@pytest.mark.parametrize("n4,blocks,reps", [(0, 4, 1), (16, 0, 1), (16, 4, 0)])
+def test_stream_copy_rejects_bad_arguments(n4, blocks, reps):
+    dummy = ctypes.c_void_p(16)  # never dereferenced: arguments are checked first
+    ms = ctypes.c_float()
+    assert _copy_lib().kbp_stream_copy_time(dummy, dummy, n4, blocks, reps, None,
+                                            ctypes.byref(ms)) == -1
 
 
 @pytest.mark.parametrize("n4,blocks,reps", [(0, 4, 1), (16, 0, 1), (16, 4, 0)])
@@ -73,3 +90,14 @@ def test_probe_sums_the_indexed_rows(b, n, chunk):
     assert ms.value > 0
     want = np.stack([X[idx[g * chunk:(g + 1) * chunk]].sum(axis=0) for g in range(n_chunks)])
     np.testing.assert_array_equal(out.cpu().numpy().reshape(n_chunks, b), want)
+
+
+@pytest.mark.gpu
+def test_stream_copy_copies():
+    import torch
+    src = torch.arange(4 * 5000, dtype=torch.float32, device="cuda")
+    dst = torch.full_like(src, float("nan"))
+    ms = ctypes.c_float()
+    assert _copy_lib().kbp_stream_copy_time(src.data_ptr(), dst.data_ptr(), 5000, 7, 2, None,
+                                            ctypes.byref(ms)) == 0
+    assert torch.equal(src, dst) and ms.value > 0
