@@ -115,6 +115,24 @@ def fingerprint(defines, path, bdir, csrc=CSRC) -> dict:
     return digests
 
 
+CHAIN_LIB = os.path.join(OUT_DIR, "libkbchain.so")
+
+
+def build_chain(verbose: bool = False) -> str:
+    """Compile the multi-hop chain glue (include/kbchain.h) into its own
+    shared library."""
+    os.makedirs(OUT_DIR, exist_ok=True)
+    tmp = CHAIN_LIB + ".tmp"
+    cmd = [hipcc(), "-x", "hip", *DEVICE_FLAGS, *COMMON_FLAGS, "-shared",
+           os.path.join(CSRC, "chain_glue.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+    os.replace(tmp, CHAIN_LIB)
+    return CHAIN_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
     print(build_probe(verbose="-v" in sys.argv))
+    print(build_chain(verbose="-v" in sys.argv))

@@ -108,34 +108,27 @@ def test_deterministic(kbf, name):
 
 
 def chain_gpu(kbf, kb, x0, rho, target):
-    """The three-hop chain with follow on the GPU; the glue (softmax, L1
-    normalisation, cross-entropy) in float64 torch ops around it."""
-    import torch
+    """The three-hop chain entirely in this project's kernels: follow and its
+    backward (libkbfollow), the softmax over relations, the per-example L1
+    normalisation and the softmax cross-entropy with their backwards
+    (libkbchain).  No torch arithmetic."""
+    from paper_2002_06115_amd import chain
     hops = len(rho)
     xs = [to_em(x0)]
     rs, sums = [], []
     for t in range(hops):
-        r = torch.softmax(to_em(rho[t]).double(), dim=0)
+        r = chain.softmax(to_em(rho[t]))
         rs.append(r)
-        u = kb.follow(xs[-1], r.float().contiguous())
-        s = u.double().sum(dim=0, keepdim=True)
+        x, s = chain.l1_normalize(kb.follow(xs[-1], r))
         sums.append(s)
-        xs.append((u.double() / s).float().contiguous())
-    z = xs[-1].double()
-    tgt = to_em(target).double()
-    logp = torch.log_softmax(z, dim=0)
-    b = z.shape[1]
-    loss = float(-(tgt * logp).sum() / b)
-    dx = ((torch.softmax(z, dim=0) - tgt) / b)
+        xs.append(x)
+    loss, _, dx = chain.softmax_xent(xs[-1], to_em(target))
     drho = [None] * hops
     for t in range(hops, 0, -1):
-        x_t = xs[t].double()
-        du = (dx - (dx * x_t).sum(dim=0, keepdim=True)) / sums[t - 1]
-        dxp, dr = kb.follow_backward(xs[t - 1], rs[t - 1].float().contiguous(), du.float().contiguous())
-        r = rs[t - 1]
-        drho[t - 1] = from_em(r * (dr.double() - (dr.double() * r).sum(dim=0, keepdim=True)))
-        dx = dxp.double()
-    return loss, from_em(dx), drho
+        du = chain.l1_normalize_backward(xs[t], sums[t - 1], dx)
+        dx, dr = kb.follow_backward(xs[t - 1], rs[t - 1], du)
+        drho[t - 1] = from_em(chain.softmax_backward(rs[t - 1], dr))
+    return float(loss), from_em(dx), drho
 
 
 def test_three_hop_chain(kbf):
