@@ -1,0 +1,157 @@
+// Host planner under AddressSanitizer and UndefinedBehaviorSanitizer: the
+// validation, the three stable counting sorts and the stream plans of
+// random, Zipf-hub, empty and degenerate KBs, with the plan's invariants
+// checked along the way.  Exit status 0 when every check holds (sanitizer
+// reports abort the program).  Built and run by tests/test_host_sanitizers.py.
+#include <cstdio>
+#include <cstdlib>
+#include <random>
+#include <vector>
+
+#include "plan.h"
+
+using namespace kbf;
+
+static int failures = 0;
+#define CHECK(cond, ...)                                  \
+  do {                                                    \
+    if (!(cond)) {                                        \
+      std::fprintf(stderr, "check failed: %s: ", #cond);  \
+      std::fprintf(stderr, __VA_ARGS__);                  \
+      std::fprintf(stderr, "\n");                         \
+      ++failures;                                         \
+    }                                                     \
+  } while (0)
+
+// Every stream property the kernels rely on.
+static void check_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk, const char *what) {
+  const int64_t n = (int64_t)P.entries.size();
+  CHECK(n % chunk == 0, "%s: %lld entries, chunk %d", what, (long long)n, chunk);
+  CHECK(P.n_chunks * chunk == n, "%s: n_chunks", what);
+  int64_t triples = 0, row_markers = 0;
+  std::vector<int> slot_written(P.n_slots, 0);
+  for (int64_t p = 0; p < n; ++p) {
+    const Entry &e = P.entries[p];
+    if (p % chunk == chunk - 1) CHECK(e.x == kMarker, "%s: chunk end %lld is no marker", what, (long long)p);
+    if (e.x == kMarker) {
+      if (e.y >= 0) {
+        CHECK(e.y < L.rows, "%s: row target %d", what, e.y);
+        ++row_markers;
+      } else if (e.y != kNoTarget) {
+        const int64_t slot = -(int64_t)e.y - 1;
+        CHECK(slot >= 0 && slot < P.n_slots, "%s: slot %lld", what, (long long)slot);
+        if (slot >= 0 && slot < P.n_slots) ++slot_written[slot];
+      }
+    } else {
+      CHECK(e.x >= 0, "%s: entry %lld", what, (long long)p);
+      ++triples;
+    }
+  }
+  CHECK(triples == (int64_t)L.col_a.size(), "%s: %lld of %zu triples in the stream", what,
+        (long long)triples, L.col_a.size());
+  int64_t non_empty = 0;
+  for (int64_t q = 0; q < L.rows; ++q) non_empty += L.offsets[q + 1] > L.offsets[q];
+  CHECK(row_markers + P.n_split_rows == non_empty, "%s: row markers", what);
+  CHECK((int64_t)P.empty_rows.size() == L.rows - non_empty, "%s: empty rows", what);
+  // Every stream slot is written once; combine outputs are later slots.
+  int64_t stream_slots = 0;
+  for (int64_t s = 0; s < P.n_slots; ++s) {
+    CHECK(slot_written[s] <= 1, "%s: slot %lld written twice", what, (long long)s);
+    stream_slots += slot_written[s];
+  }
+  int64_t tasks_to_rows = 0;
+  for (const auto &level : P.levels)
+    for (const CombineTask &t : level) {
+      CHECK(t.n >= 1 && t.n <= P.fan_in, "%s: task of %d slots", what, t.n);
+      CHECK(t.first >= 0 && t.first + t.n <= P.n_slots, "%s: task range", what);
+      if (t.dst >= 0) {
+        CHECK(t.dst < L.rows, "%s: task row", what);
+        ++tasks_to_rows;
+      } else {
+        CHECK(-(int64_t)t.dst - 1 < P.n_slots, "%s: task slot", what);
+      }
+    }
+  CHECK(tasks_to_rows == P.n_split_rows, "%s: final combine tasks", what);
+  if (!P.weights.empty()) CHECK(P.weights.size() == P.entries.size(), "%s: weights", what);
+}
+
+static void check_layout(const LayoutHost &L, int64_t n_t, const char *what) {
+  CHECK((int64_t)L.col_a.size() == n_t && (int64_t)L.col_b.size() == n_t, "%s: sizes", what);
+  CHECK((int64_t)L.offsets.size() == L.rows + 1 && L.offsets[0] == 0 && L.offsets[L.rows] == n_t,
+        "%s: offsets", what);
+  for (int64_t q = 0; q < L.rows; ++q) {
+    CHECK(L.offsets[q] <= L.offsets[q + 1], "%s: offsets not monotone", what);
+    for (int32_t p = L.offsets[q] + 1; p < L.offsets[q + 1]; ++p)
+      CHECK(L.col_b[p - 1] <= L.col_b[p], "%s: runs not sorted in row %lld", what, (long long)q);
+  }
+}
+
+static void run_case(const char *what, int64_t n_e, int64_t n_r, std::vector<int32_t> s,
+                     std::vector<int32_t> r, std::vector<int32_t> o, bool weighted) {
+  const int64_t n_t = (int64_t)s.size();
+  bool range = false;
+  CHECK(validate_triples(n_e, n_r, n_t, s.data(), r.data(), o.data(), &range).empty(),
+        "%s: valid triples refused", what);
+  std::vector<float> w;
+  if (weighted) {
+    w.resize(n_t);
+    for (int64_t l = 0; l < n_t; ++l) w[l] = 0.5f + (float)(l % 7);
+  }
+  LayoutHost L[3];
+  build_layouts(n_e, n_r, n_t, s.data(), r.data(), o.data(), weighted ? w.data() : nullptr, true, L);
+  for (int k = 0; k < 3; ++k) {
+    check_layout(L[k], n_t, what);
+    for (int32_t chunk : {16, 24, 256}) {
+      for (int32_t fan_in : {2, 3, 32}) check_plan(L[k], plan_layout(L[k], chunk, fan_in), chunk, what);
+    }
+  }
+}
+
+int main() {
+  std::mt19937_64 g(20020615);
+  // Invalid arguments: each refused with a message, range errors flagged.
+  {
+    std::vector<int32_t> s = {0, 5}, r = {0, 0}, o = {1, 1};
+    bool range = false;
+    CHECK(!validate_triples(5, 1, 2, s.data(), r.data(), o.data(), &range).empty() && range,
+          "subject id == N_E accepted");
+    CHECK(!validate_triples(-1, 1, 0, nullptr, nullptr, nullptr, &range).empty() && !range,
+          "negative N_E accepted");
+    CHECK(!validate_triples(5, 1, 2, nullptr, r.data(), o.data(), &range).empty(),
+          "null subj accepted");
+    CHECK(!validate_triples((1 << 30) + 1, 1, 0, nullptr, nullptr, nullptr, &range).empty(),
+          "N_E above 2^30 accepted");
+  }
+  // Random KBs.
+  for (int rep = 0; rep < 4; ++rep) {
+    const int64_t n_e = 50 + rep * 300, n_r = 1 + rep * 3, n_t = 2000 + rep * 5000;
+    std::uniform_int_distribution<int32_t> E(0, (int32_t)n_e - 1), R(0, (int32_t)n_r - 1);
+    std::vector<int32_t> s(n_t), r(n_t), o(n_t);
+    for (int64_t l = 0; l < n_t; ++l) {
+      s[l] = E(g);
+      r[l] = R(g);
+      o[l] = E(g);
+    }
+    run_case("random", n_e, n_r, s, r, o, rep % 2 == 1);
+  }
+  // One hub holding every triple, beside empty rows; duplicate triples.
+  {
+    const int64_t n_t = 20000;
+    std::vector<int32_t> s(n_t, 3), r(n_t), o(n_t);
+    for (int64_t l = 0; l < n_t; ++l) {
+      r[l] = (int32_t)(l % 2);
+      o[l] = (int32_t)(l % 5);
+    }
+    run_case("hub", 10, 2, s, r, o, true);
+  }
+  // Empty KB; one entity with self-loops; one relation.
+  run_case("empty", 7, 3, {}, {}, {}, false);
+  run_case("self loops", 1, 1, std::vector<int32_t>(100, 0), std::vector<int32_t>(100, 0),
+           std::vector<int32_t>(100, 0), false);
+  if (failures) {
+    std::fprintf(stderr, "%d checks failed\n", failures);
+    return 1;
+  }
+  std::printf("planner checks passed\n");
+  return 0;
+}
