@@ -197,6 +197,21 @@ kb_status kb_layout_host(int64_t n_entities, int64_t n_relations, int64_t n_trip
                          int32_t *perm);
 
 /* ------------------------------------------------------------------------
+ * Checked builds (for testing)
+ * ------------------------------------------------------------------------ */
+
+/*
+ * A build compiled with KBFOLLOW_CHECKED validates, inside the kernels, every
+ * row, workspace-slot and combine index against its table before using it.
+ * An index outside its table is replaced by a valid one and counted; the
+ * computation goes on (results are then wrong, but no access leaves its
+ * buffer).  This returns the count on the current device since the last
+ * reset (and resets it when `reset` is nonzero).  Normal builds return
+ * KB_ENOTSUP with *count = 0.
+ */
+kb_status kb_checked_violations(uint64_t *count, int32_t reset);
+
+/* ------------------------------------------------------------------------
  * Kernel timing with HIP events (for benchmarks; not thread safe)
  * ------------------------------------------------------------------------ */
 

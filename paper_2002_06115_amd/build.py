@@ -68,6 +68,17 @@ def build(verbose: bool = False, defines=(), out=None, build_dir=None, src_dir=N
     return out
 
 
+CHECKED_LIB = os.path.join(OUT_DIR, "checked", "libkbfollow.so")
+
+
+def build_checked(verbose: bool = False) -> str:
+    """The follow library with in-kernel index validation (KBFOLLOW_CHECKED),
+    for tests: every row, slot and combine index is checked before use and
+    violations are counted (kb_checked_violations)."""
+    return build(verbose, defines=("KBFOLLOW_CHECKED",), out=CHECKED_LIB,
+                 build_dir=os.path.join(BUILD_DIR, "checked"))
+
+
 PROBE_LIB = os.path.join(OUT_DIR, "libkbprobe.so")
 
 
@@ -136,3 +147,4 @@ if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
     print(build_probe(verbose="-v" in sys.argv))
     print(build_chain(verbose="-v" in sys.argv))
+    print(build_checked(verbose="-v" in sys.argv))

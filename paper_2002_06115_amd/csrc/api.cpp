@@ -212,13 +212,14 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
     PhaseScope scope(kb, ph_base + 1, s);
     for (size_t L = 0; L + 1 < D.level_begin.size(); ++L) {
       const int64_t n = D.level_begin[L + 1] - D.level_begin[L];
-      hipError_t e = launch_combine(D.ctasks + D.level_begin[L], n, slots, b, out, res, gamma, s);
+      hipError_t e = launch_combine(D.ctasks + D.level_begin[L], n, slots, D.n_slots, b, out,
+                                    D.rows, res, gamma, s);
       if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
     }
   }
   {
     PhaseScope scope(kb, ph_base + 2, s);
-    hipError_t e = launch_zero_rows(D.empty, D.n_empty, b, out, res, gamma, s);
+    hipError_t e = launch_zero_rows(D.empty, D.n_empty, b, out, D.rows, res, gamma, s);
     if (e != hipSuccess) return hip_fail(e, "zero-rows kernel launch");
   }
   return KB_OK;
@@ -498,6 +499,18 @@ kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const fl
                              const float *dY, float *dX, float *dR, void *workspace,
                              size_t ws_bytes, void *stream) {
   return backward_impl(kb, b, X, R, dY, false, 0.0f, dX, dR, workspace, ws_bytes, stream);
+}
+
+kb_status kb_checked_violations(uint64_t *count, int32_t reset) {
+  if (!count) return fail(KB_EINVAL, "count must be non-NULL");
+  *count = 0;
+  unsigned long long c = 0;
+  hipError_t e = checked_violations(&c, reset != 0);
+  if (e == hipErrorNotSupported)
+    return fail(KB_ENOTSUP, "this build has no bounds checks (build with KBFOLLOW_CHECKED)");
+  if (e != hipSuccess) return hip_fail(e, "reading the violation counter");
+  *count = c;
+  return KB_OK;
 }
 
 kb_status kb_profile_enable(kb_t *kb, int32_t on) {

@@ -54,12 +54,17 @@ hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s);
 
 // Sums workspace slots in order (one combine level).  A final row write adds
 // gamma * res[row] when res is not null (residual hop).
-hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int32_t b,
-                          float *out, const float *res, float gamma, hipStream_t s);
+hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int64_t n_slots,
+                          int32_t b, float *out, int64_t out_rows, const float *res, float gamma,
+                          hipStream_t s);
 
 // Writes +0.0 to the listed rows of out ([rows][b]), or gamma * res[row] when
 // res is not null (residual hop).
 hipError_t launch_zero_rows(const int32_t *rows, int64_t n_rows, int32_t b, float *out,
-                            const float *res, float gamma, hipStream_t s);
+                            int64_t out_rows, const float *res, float gamma, hipStream_t s);
+
+// Bounds violations counted by a checked build (KBFOLLOW_CHECKED) on the
+// current device since the last reset; hipErrorNotSupported otherwise.
+hipError_t checked_violations(unsigned long long *count, bool reset);
 
 }  // namespace kbf

@@ -47,6 +47,23 @@ static_assert(kChunkQuantum % kUnroll == 0, "a chunk is a whole number of steps"
 constexpr int kRawBufferWord3 = 0x00020000;
 constexpr uint32_t kOutOfRange = 0xFFFFFFF0u;
 
+// Checked builds (KBFOLLOW_CHECKED) validate every row, slot and combine
+// index before it is used: KBF_CHECKED(i, n) is i when 0 <= i < n, else 0 (a
+// valid index) with one more count in a device-wide counter, so a planning
+// bug shows up as a count instead of an out-of-bounds access.  In normal
+// builds KBF_CHECKED(i, n) is just (i): the same code as without checks.
+#ifdef KBFOLLOW_CHECKED
+__device__ unsigned long long g_violations;
+__device__ __forceinline__ int64_t checked(int64_t i, int64_t n) {
+  if (i >= 0 && i < n) return i;
+  atomicAdd(&g_violations, 1ull);
+  return 0;
+}
+#define KBF_CHECKED(i, n) checked((i), (n))
+#else
+#define KBF_CHECKED(i, n) (i)
+#endif
+
 template <class F, int... I>
 __device__ __forceinline__ void static_for_impl(F &f, std::integer_sequence<int, I...>) {
   (f(std::integral_constant<int, I>{}), ...);
@@ -264,14 +281,21 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
         const bool res_row = RES && !triple && e[u].y >= 0;
         const uint32_t ia = triple ? (uint32_t)(e[u].x & kIdMask) : (uint32_t)e[u].y;
         if constexpr (BUF) {
-          load_row_buffer<VEC>(arsrc, (triple || res_row) ? ia * row_bytes + col_bytes : kOutOfRange,
+          load_row_buffer<VEC>(arsrc,
+                               (triple || res_row)
+                                   ? (uint32_t)KBF_CHECKED(ia, a.A_rows) * row_bytes + col_bytes
+                                   : kOutOfRange,
                                xa[u]);
-          load_row_buffer<VEC>(brsrc, run_start ? (uint32_t)e[u].y * row_bytes + col_bytes
-                                                : kOutOfRange,
+          load_row_buffer<VEC>(brsrc,
+                               run_start ? (uint32_t)KBF_CHECKED(e[u].y, a.B_rows) * row_bytes +
+                                               col_bytes
+                                         : kOutOfRange,
                                xb[u]);
         } else {
-          load_row<VEC>(a.A + (size_t)(triple || res_row ? ia : 0) * bb + cl, xa[u]);
-          load_row<VEC>(a.B + (size_t)(run_start ? e[u].y : 0) * bb + cl, xb[u]);
+          load_row<VEC>(a.A + (size_t)(triple || res_row ? KBF_CHECKED(ia, a.A_rows) : 0) * bb + cl,
+                        xa[u]);
+          load_row<VEC>(a.B + (size_t)(run_start ? KBF_CHECKED(e[u].y, a.B_rows) : 0) * bb + cl,
+                        xb[u]);
         }
       }
       fetch(p + kUnroll, mine_next, wmine_next);
@@ -300,16 +324,19 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
             y[v] = (RES && f >= 0) ? acc[v] + (double)a.gamma * (double)xa[u][v] : acc[v];
           if (f >= 0) {
             if constexpr (BUF)
-              store_row_buffer<VEC>(orsrc, (uint32_t)f * row_bytes + col_bytes, y);
+              store_row_buffer<VEC>(
+                  orsrc, (uint32_t)KBF_CHECKED(f, a.out_rows) * row_bytes + col_bytes, y);
             else
-              store_row<VEC>(a.out + (size_t)f * bb + c, y);
+              store_row<VEC>(a.out + (size_t)KBF_CHECKED(f, a.out_rows) * bb + c, y);
           } else {
             if constexpr (BUF)
-              store_slot_buffer<VEC>(srsrc, ((uint32_t)(-(f + 1)) * (uint32_t)a.b + (uint32_t)c) *
-                                                (uint32_t)sizeof(double),
-                                     y);
+              store_slot_buffer<VEC>(
+                  srsrc,
+                  ((uint32_t)KBF_CHECKED(-(f + 1), a.n_slots) * (uint32_t)a.b + (uint32_t)c) *
+                      (uint32_t)sizeof(double),
+                  y);
             else
-              store_slot<VEC>(a.slots + (size_t)(-(f + 1)) * bb + c, y);
+              store_slot<VEC>(a.slots + (size_t)KBF_CHECKED(-(f + 1), a.n_slots) * bb + c, y);
           }
         }
 #pragma unroll
@@ -324,8 +351,9 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
 template <int VEC, int LPT>
 __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict__ tasks,
                                                          int64_t n_tasks,
-                                                         double *__restrict__ slots, int32_t b,
-                                                         float *__restrict__ out,
+                                                         double *__restrict__ slots,
+                                                         int64_t n_slots, int32_t b,
+                                                         float *__restrict__ out, int64_t out_rows,
                                                          const float *__restrict__ res,
                                                          float gamma) {
   constexpr int W = LPT * VEC;
@@ -346,7 +374,8 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
       double part[kUnroll][VEC];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
-        load_slot<VEC>(slots + (size_t)(tk.x + i + min(u, n - 1)) * bb + c, part[u]);
+        load_slot<VEC>(slots + (size_t)KBF_CHECKED(tk.x + i + min(u, n - 1), n_slots) * bb + c,
+                       part[u]);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
         if (u < n) {
@@ -355,15 +384,16 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
         }
     }
     if (tk.z >= 0) {
+      const size_t row = (size_t)KBF_CHECKED(tk.z, out_rows);
       if (res) {
         float r[VEC];
-        load_row<VEC>(res + (size_t)tk.z * bb + c, r);
+        load_row<VEC>(res + row * bb + c, r);
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[v] += (double)gamma * (double)r[v];
       }
-      store_row<VEC>(out + (size_t)tk.z * bb + c, acc);
+      store_row<VEC>(out + row * bb + c, acc);
     } else {
-      store_slot<VEC>(slots + (size_t)(-(tk.z + 1)) * bb + c, acc);
+      store_slot<VEC>(slots + (size_t)KBF_CHECKED(-(int64_t)tk.z - 1, n_slots) * bb + c, acc);
     }
   }
 }
@@ -372,6 +402,7 @@ template <int VEC>
 __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__restrict__ rows,
                                                            int64_t n_rows, int32_t b,
                                                            float *__restrict__ out,
+                                                           int64_t out_rows,
                                                            const float *__restrict__ res,
                                                            float gamma) {
   const int per_row = b / VEC;
@@ -380,7 +411,7 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__rest
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
     const int64_t q = e / per_row;
     const int j = (int)(e - q * per_row);
-    const size_t off = (size_t)rows[q] * (size_t)b + (size_t)j * VEC;
+    const size_t off = (size_t)KBF_CHECKED(rows[q], out_rows) * (size_t)b + (size_t)j * VEC;
     double y[VEC];
     if (res) {
       float r[VEC];
@@ -477,30 +508,48 @@ hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 
-hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int32_t b,
-                          float *out, const float *res, float gamma, hipStream_t s) {
+hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int64_t n_slots,
+                          int32_t b, float *out, int64_t out_rows, const float *res, float gamma,
+                          hipStream_t s) {
   if (n_tasks == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(b);
   const void *fn = t.vec == 4 ? combine_fn<4>(t.lpt) : combine_fn<1>(t.lpt);
   if (!fn) return hipErrorInvalidValue;
   const dim3 grid((unsigned)blocks_for(n_tasks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
-  void *params[] = {&tasks, &n_tasks, &slots, &b, &out, &res, &gamma};
+  void *params[] = {&tasks, &n_tasks, &slots, &n_slots, &b, &out, &out_rows, &res, &gamma};
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 
 hipError_t launch_zero_rows(const int32_t *rows, int64_t n_rows, int32_t b, float *out,
-                            const float *res, float gamma, hipStream_t s) {
+                            int64_t out_rows, const float *res, float gamma, hipStream_t s) {
   if (n_rows == 0) return hipSuccess;
   const int vec = (b % 4 == 0) ? 4 : 1;
   const int64_t items = n_rows * (b / vec);
   const dim3 grid((unsigned)blocks_for(items, kBlock, 256 * 64));
   if (vec == 4)
-    hipLaunchKernelGGL(zero_rows_kernel<4>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, res,
+    hipLaunchKernelGGL(zero_rows_kernel<4>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, out_rows, res,
                        gamma);
   else
-    hipLaunchKernelGGL(zero_rows_kernel<1>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, res,
+    hipLaunchKernelGGL(zero_rows_kernel<1>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, out_rows, res,
                        gamma);
   return hipGetLastError();
+}
+
+}  // namespace kbf
+
+namespace kbf {
+
+hipError_t checked_violations(unsigned long long *count, bool reset) {
+#ifdef KBFOLLOW_CHECKED
+  hipError_t e = hipMemcpyFromSymbol(count, HIP_SYMBOL(g_violations), sizeof *count);
+  if (e != hipSuccess || !reset) return e;
+  const unsigned long long zero = 0;
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_violations), &zero, sizeof zero);
+#else
+  (void)count;
+  (void)reset;
+  return hipErrorNotSupported;
+#endif
 }
 
 }  // namespace kbf

@@ -40,6 +40,21 @@ def test_library_exports_every_declared_symbol(kbf):
         assert hasattr(lib, name), name
 
 
+def test_normal_build_has_no_bounds_checks(kbf):
+    count = ctypes.c_uint64(7)
+    lib = kbf._lib
+    lib.kb_checked_violations.argtypes = [ctypes.POINTER(ctypes.c_uint64), ctypes.c_int32]
+    assert lib.kb_checked_violations(ctypes.byref(count), 0) == kbf.KB_ENOTSUP
+    assert count.value == 0
+
+
+def test_checked_build_exports_every_declared_symbol():
+    from paper_2002_06115_amd import build as kbuild
+    lib = ctypes.CDLL(kbuild.CHECKED_LIB)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
 def test_status_strings(kbf):
     lib = kbf._lib
     assert lib.kb_status_str(0) == b"ok"
