@@ -1,0 +1,70 @@
+"""Every kernel variant against the oracle.
+
+The stream kernel is instantiated per lane layout (4 floats per lane when
+b % 4 == 0, else 1; lane groups of 1..64 lanes; column slices beyond 256
+columns), per load path (raw buffer loads, or plain loads as for tables of
+4 GB or more), per hard or soft KB (App. A weights) and per plain or residual
+hop (Sec. 3.2, App. E).  Each combination runs forward and backward on a KB
+with 16-entry chunks (rows split over many chunks, deep combine trees, runs
+cut by chunk ends) and is compared elementwise with the oracle.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import assert_close, from_em, to_em
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kbf():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2002_06115_amd as kbf
+    return kbf
+
+
+def small_kb(seed, n_e=300, n_r=7, n_t=6000):
+    g = np.random.default_rng(seed)
+    # A few hub subjects and objects beside uniform ones.
+    s = np.where(g.random(n_t) < 0.3, g.integers(0, 3, n_t), g.integers(0, n_e, n_t))
+    o = np.where(g.random(n_t) < 0.3, g.integers(0, 3, n_t), g.integers(0, n_e, n_t))
+    r = g.integers(0, n_r, n_t)
+    return s.astype(np.int32), r.astype(np.int32), o.astype(np.int32), n_e, n_r
+
+
+COMBOS = list(itertools.product([1, 4, 5, 36, 260], [False, True], [None, 0.5], [False, True]))
+
+
+@pytest.mark.parametrize("b,weighted,gamma,plain", COMBOS)
+def test_variant(kbf, b, weighted, gamma, plain, monkeypatch):
+    monkeypatch.setenv("KBFOLLOW_CHUNK", "16")
+    monkeypatch.setenv("KBFOLLOW_REL_CHUNK", "16")
+    monkeypatch.setenv("KBFOLLOW_FAN_IN", "3")
+    if plain:
+        monkeypatch.setenv("KBFOLLOW_PLAIN_LOADS", "1")
+    s, r, o, n_e, n_r = small_kb(b * 7 + weighted)
+    g = np.random.default_rng(b)
+    w = g.uniform(0.1, 2.0, len(s)).astype(np.float32) if weighted else None
+    X = g.standard_normal((b, n_e)).astype(np.float32)
+    R = g.standard_normal((b, n_r)).astype(np.float32)
+    dY = g.standard_normal((b, n_e)).astype(np.float32)
+    kb = kbf.KB(s, r, o, n_e, n_r, weight=w)
+    Y = from_em(kb.follow(to_em(X), to_em(R), residual=gamma))
+    dX, dR = kb.follow_backward(to_em(X), to_em(R), to_em(dY), residual=gamma)
+    if gamma is None:
+        wantY = oracle.follow(s, r, o, n_e, n_r, X, R, weight=w)
+        wantdX, wantdR = oracle.follow_backward(s, r, o, n_e, n_r, X, R, dY, weight=w)
+    else:
+        wantY = oracle.follow_residual(s, r, o, n_e, n_r, X, R, gamma=gamma, weight=w)
+        wantdX, wantdR = oracle.follow_backward_residual(s, r, o, n_e, n_r, X, R, dY,
+                                                         gamma=gamma, weight=w)
+    label = f"b={b} weighted={weighted} gamma={gamma} plain={plain}"
+    assert_close(Y, wantY, label + " Y")
+    assert_close(from_em(dX), wantdX, label + " dX")
+    assert_close(from_em(dR), wantdR, label + " dR")
+    kb.close()
