@@ -39,8 +39,9 @@ struct DevLayout {
   int64_t n = 0;
   int32_t chunk = 0;
   int64_t n_chunks = 0;
-  int32_t *empty = nullptr;
-  int64_t n_empty = 0;
+  int2 *empty = nullptr;      // pieces (first row, count) of rows no triple reaches
+  int64_t n_empty_pieces = 0;
+  int64_t n_empty = 0;        // rows in those pieces
   int4 *ctasks = nullptr;     // all combine levels, back to back
   std::vector<int64_t> level_begin;  // host: level L is [level_begin[L], level_begin[L+1])
   int64_t n_slots = 0;
@@ -116,7 +117,8 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
   D.n = (int64_t)P.entries.size();
   D.chunk = chunk;
   D.n_chunks = P.n_chunks;
-  D.n_empty = (int64_t)P.empty_rows.size();
+  D.n_empty = P.n_empty_rows;
+  D.n_empty_pieces = (int64_t)P.empty.size();
   D.n_slots = P.n_slots;
   D.n_split_rows = P.n_split_rows;
   D.max_row_len = P.max_row_len;
@@ -133,7 +135,11 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
   kb_status st;
   if ((st = upload(kb, entries, &D.entries, s)) != KB_OK) return st;
   if ((st = upload(kb, P.weights, &D.weights, s)) != KB_OK) return st;
-  if ((st = upload(kb, P.empty_rows, &D.empty, s)) != KB_OK) return st;
+  static_assert(sizeof(EmptyPiece) == sizeof(int2), "empty-piece layout");
+  std::vector<int2> pieces(P.empty.size());
+  if (!pieces.empty()) std::memcpy(pieces.data(), P.empty.data(), pieces.size() * sizeof(int2));
+  std::vector<EmptyPiece>().swap(P.empty);
+  if ((st = upload(kb, pieces, &D.empty, s)) != KB_OK) return st;
   if ((st = upload(kb, ctasks, &D.ctasks, s)) != KB_OK) return st;
   // The host vectors die with this frame: wait for the copies first.
   hipError_t e = hipStreamSynchronize(s);
@@ -219,7 +225,7 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
   }
   {
     PhaseScope scope(kb, ph_base + 2, s);
-    hipError_t e = launch_zero_rows(D.empty, D.n_empty, b, out, D.rows, res, gamma, s);
+    hipError_t e = launch_zero_rows(D.empty, D.n_empty_pieces, b, out, D.rows, res, gamma, s);
     if (e != hipSuccess) return hip_fail(e, "zero-rows kernel launch");
   }
   return KB_OK;
@@ -278,7 +284,7 @@ kb_status kb_layout_host(int64_t n_entities, int64_t n_relations, int64_t n_trip
     std::string msg = validate_triples(n_entities, n_relations, n_triples, subj, rel, obj, &range);
     if (!msg.empty()) return fail(range ? KB_ERANGE : KB_EINVAL, msg);
     LayoutHost L[3];
-    build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, nullptr, true, L);
+    build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, nullptr, true, true, L);
     const LayoutHost &H = L[which];
     if (offsets) std::copy(H.offsets.begin(), H.offsets.end(), offsets);
     if (col_a) std::copy(H.col_a.begin(), H.col_a.end(), col_a);
@@ -337,7 +343,7 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
     {
       LayoutHost H[3];
-      build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, weight, false, H);
+      build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, weight, false, false, H);
       const int32_t plen[3] = {chunk_seg, chunk_seg, chunk_rel};
       for (int k = 0; k < 3; ++k) {
         kb_status st = build_device_layout(kb, kb->L[k], H[k], plen[k], fan_in, s);
@@ -345,7 +351,7 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
           free_kb(kb);
           return st;
         }
-        std::vector<int32_t>().swap(H[k].offsets);
+        std::vector<int32_t>().swap(H[k].row);
         std::vector<int32_t>().swap(H[k].col_a);
         std::vector<int32_t>().swap(H[k].col_b);
         std::vector<float>().swap(H[k].weight);

@@ -58,9 +58,9 @@ hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int
                           int32_t b, float *out, int64_t out_rows, const float *res, float gamma,
                           hipStream_t s);
 
-// Writes +0.0 to the listed rows of out ([rows][b]), or gamma * res[row] when
-// res is not null (residual hop).
-hipError_t launch_zero_rows(const int32_t *rows, int64_t n_rows, int32_t b, float *out,
+// Writes +0.0 to the rows of out ([out_rows][b]) in the given pieces (first
+// row, count), or gamma * res[row] when res is not null (residual hop).
+hipError_t launch_zero_rows(const int2 *pieces, int64_t n_pieces, int32_t b, float *out,
                             int64_t out_rows, const float *res, float gamma, hipStream_t s);
 
 // Bounds violations counted by a checked build (KBFOLLOW_CHECKED) on the

@@ -398,33 +398,41 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
   }
 }
 
-template <int VEC>
-__global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int32_t *__restrict__ rows,
-                                                           int64_t n_rows, int32_t b,
+// Writes the rows no triple reaches: one lane group per piece of consecutive
+// rows (first, count), lanes over the columns as in the stream kernel.
+template <int VEC, int LPT>
+__global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int2 *__restrict__ pieces,
+                                                           int64_t n_pieces, int32_t b,
                                                            float *__restrict__ out,
                                                            int64_t out_rows,
                                                            const float *__restrict__ res,
                                                            float gamma) {
-  const int per_row = b / VEC;
-  const int64_t total = n_rows * per_row;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
-    const int64_t q = e / per_row;
-    const int j = (int)(e - q * per_row);
-    const size_t off = (size_t)KBF_CHECKED(rows[q], out_rows) * (size_t)b + (size_t)j * VEC;
-    double y[VEC];
-    if (res) {
-      float r[VEC];
-      load_row<VEC>(res + off, r);
+  constexpr int W = LPT * VEC;
+  constexpr int GPB = kBlock / LPT;
+  const int lane = threadIdx.x % LPT;
+  const int grp = threadIdx.x / LPT;
+  const int c = blockIdx.y * W + lane * VEC;
+  if (c >= b) return;  // no barrier below
+  const size_t bb = (size_t)b;
+  const int64_t stride = (int64_t)gridDim.x * GPB;
+  for (int64_t t = (int64_t)blockIdx.x * GPB + grp; t < n_pieces; t += stride) {
+    const int2 pc = pieces[t];  // first row, count
+    for (int i = 0; i < pc.y; ++i) {
+      const size_t off = (size_t)KBF_CHECKED((int64_t)pc.x + i, out_rows) * bb + c;
+      double y[VEC];
+      if (res) {
+        float r[VEC];
+        load_row<VEC>(res + off, r);
 #pragma unroll
-      for (int v = 0; v < VEC; ++v) y[v] = 0.0 + (double)gamma * (double)r[v];
-    } else {
+        for (int v = 0; v < VEC; ++v) y[v] = 0.0 + (double)gamma * (double)r[v];
+      } else {
 #pragma unroll
-      for (int v = 0; v < VEC; ++v) y[v] = 0.0;
+        for (int v = 0; v < VEC; ++v) y[v] = 0.0;
+      }
+      // Non-temporal, like every output row: plain stores would leave the
+      // rows dirty in the caches, to be written back during the next pass.
+      store_row<VEC>(out + off, y);
     }
-    // Non-temporal, like every output row: plain stores would leave the
-    // rows dirty in the caches, to be written back during the next pass.
-    store_row<VEC>(out + off, y);
   }
 }
 
@@ -464,6 +472,20 @@ const void *combine_fn(int lpt) {
     case 16: return reinterpret_cast<const void *>(&combine_kernel<VEC, 16>);
     case 32: return reinterpret_cast<const void *>(&combine_kernel<VEC, 32>);
     case 64: return reinterpret_cast<const void *>(&combine_kernel<VEC, 64>);
+  }
+  return nullptr;
+}
+
+template <int VEC>
+const void *zero_fn(int lpt) {
+  switch (lpt) {
+    case 1: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 1>);
+    case 2: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 2>);
+    case 4: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 4>);
+    case 8: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 8>);
+    case 16: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 16>);
+    case 32: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 32>);
+    case 64: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 64>);
   }
   return nullptr;
 }
@@ -520,24 +542,18 @@ hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 
-hipError_t launch_zero_rows(const int32_t *rows, int64_t n_rows, int32_t b, float *out,
+hipError_t launch_zero_rows(const int2 *pieces, int64_t n_pieces, int32_t b, float *out,
                             int64_t out_rows, const float *res, float gamma, hipStream_t s) {
-  if (n_rows == 0) return hipSuccess;
-  const int vec = (b % 4 == 0) ? 4 : 1;
-  const int64_t items = n_rows * (b / vec);
-  const dim3 grid((unsigned)blocks_for(items, kBlock, 256 * 64));
-  if (vec == 4)
-    hipLaunchKernelGGL(zero_rows_kernel<4>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, out_rows, res,
-                       gamma);
-  else
-    hipLaunchKernelGGL(zero_rows_kernel<1>, grid, dim3(kBlock), 0, s, rows, n_rows, b, out, out_rows, res,
-                       gamma);
-  return hipGetLastError();
+  if (n_pieces == 0) return hipSuccess;
+  const ColumnTiling t = column_tiling(b);
+  const void *fn = t.vec == 4 ? zero_fn<4>(t.lpt) : zero_fn<1>(t.lpt);
+  if (!fn) return hipErrorInvalidValue;
+  // One piece per lane group: each piece's row range is then the only load
+  // in front of its stores.
+  const dim3 grid((unsigned)blocks_for(n_pieces, kBlock / t.lpt, 0), (unsigned)t.n_slices);
+  void *params[] = {&pieces, &n_pieces, &b, &out, &out_rows, &res, &gamma};
+  return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
-
-}  // namespace kbf
-
-namespace kbf {
 
 hipError_t checked_violations(unsigned long long *count, bool reset) {
 #ifdef KBFOLLOW_CHECKED

@@ -2,8 +2,11 @@
 //
 // The reified KB of Sec. 2.3 keeps, per triple, its subject, object and
 // relation ids (the one nonzero of row l in M_subj, M_obj and M_rel).  Here
-// the triples are sorted three ways with stable counting sorts (O(N_T + N)
-// each): by (o, r, s), by (s, r, o) and by (r, s, o).  The secondary key
+// the triples are sorted three ways with stable sorts: by (o, r, s), by
+// (s, r, o) and by (r, s, o) -- counting sorts over dense id spaces,
+// comparison sorts where the id space is far larger than the KB -- and the
+// plans are built from the sorted rows alone, so building a KB costs
+// O(N_T + number of empty-row ranges) beyond the counting sorts.  The secondary key
 // groups each row into runs of equal second operand (the relation for the
 // forward and dX passes, the subject for dR), so the kernels read that
 // operand once per run instead of once per triple.
@@ -37,29 +40,50 @@ std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_
   return "";
 }
 
-// Stable counting sort of the triple ids in `in` by key[id], key in [0, n_keys).
-static void counting_sort(const int32_t *key, int64_t n_keys, const std::vector<int32_t> &in,
-                          std::vector<int32_t> &out, std::vector<int32_t> *offsets) {
-  std::vector<int64_t> start(n_keys + 1, 0);
-  for (int32_t id : in) ++start[key[id] + 1];
-  for (int64_t k = 0; k < n_keys; ++k) start[k + 1] += start[k];
-  if (offsets) {
-    offsets->resize(n_keys + 1);
-    for (int64_t k = 0; k <= n_keys; ++k) (*offsets)[k] = (int32_t)start[k];
-  }
+// Stable sort of the triple ids in `in` by key[id], key in [0, n_keys), and,
+// when `offsets` is given, the row boundaries: (*offsets)[k] = the first
+// position with key >= k, for k = 0 .. n_keys.  A counting sort (O(n +
+// n_keys), `count` is its reusable scratch) where the key space is comparable
+// to the number of ids; a stable comparison sort (O(n log n)) where it is far
+// larger, so that a KB of a few triples over 2^30 entity ids costs no pass
+// over the whole id space except the offsets themselves.
+static void sort_by_key(const int32_t *key, int64_t n_keys, const std::vector<int32_t> &in,
+                        std::vector<int32_t> &out, std::vector<int32_t> *offsets,
+                        std::vector<int32_t> &count) {
+  const int64_t n = (int64_t)in.size();
   out.resize(in.size());
-  for (int32_t id : in) out[start[key[id]]++] = id;
+  if (n_keys > 8 * n + 1024) {
+    out = in;
+    std::stable_sort(out.begin(), out.end(),
+                     [key](int32_t a, int32_t b) { return key[a] < key[b]; });
+    if (offsets) {
+      offsets->resize(n_keys + 1);
+      int64_t p = 0;
+      for (int64_t k = 0; k <= n_keys; ++k) {
+        while (p < n && key[out[p]] < k) ++p;
+        (*offsets)[k] = (int32_t)p;
+      }
+    }
+    return;
+  }
+  count.assign(n_keys + 1, 0);  // n < 2^31, so every count and prefix fits int32
+  for (int32_t id : in) ++count[key[id] + 1];
+  for (int64_t k = 0; k < n_keys; ++k) count[k + 1] += count[k];
+  if (offsets) offsets->assign(count.begin(), count.begin() + (n_keys + 1));
+  for (int32_t id : in) out[count[key[id]]++] = id;
 }
 
 static void fill_layout(LayoutHost &L, int64_t rows, std::vector<int32_t> &&order,
-                        std::vector<int32_t> &&offsets, const int32_t *a, const int32_t *b,
-                        const float *weight, bool keep_perm) {
+                        std::vector<int32_t> &&offsets, const int32_t *key, const int32_t *a,
+                        const int32_t *b, const float *weight, bool keep_perm) {
   L.rows = rows;
   L.offsets = std::move(offsets);
   const size_t n = order.size();
+  L.row.resize(n);
   L.col_a.resize(n);
   L.col_b.resize(n);
   for (size_t p = 0; p < n; ++p) {
+    L.row[p] = key[order[p]];
     L.col_a[p] = a[order[p]];
     L.col_b[p] = b[order[p]];
   }
@@ -72,31 +96,39 @@ static void fill_layout(LayoutHost &L, int64_t rows, std::vector<int32_t> &&orde
 
 void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                    const int32_t *subj, const int32_t *rel, const int32_t *obj,
-                   const float *weight, bool keep_perm, LayoutHost out[3]) {
-  std::vector<int32_t> ident(n_triples), t1, t2, by_subj, by_obj, by_rel;
+                   const float *weight, bool keep_perm, bool keep_offsets, LayoutHost out[3]) {
+  std::vector<int32_t> ident(n_triples), t1, t2, by_subj, by_obj, by_rel, count;
   for (int64_t l = 0; l < n_triples; ++l) ident[l] = (int32_t)l;
   std::vector<int32_t> off_subj, off_obj, off_rel;
   // Least significant key first; every pass is stable.
   // (s, r, o): by subject, relation runs inside a row, objects ascending.
-  counting_sort(obj, n_entities, ident, t1, nullptr);
-  counting_sort(rel, n_relations, t1, t2, nullptr);
-  counting_sort(subj, n_entities, t2, by_subj, &off_subj);
+  sort_by_key(obj, n_entities, ident, t1, nullptr, count);
+  sort_by_key(rel, n_relations, t1, t2, nullptr, count);
+  sort_by_key(subj, n_entities, t2, by_subj, keep_offsets ? &off_subj : nullptr, count);
   // (r, s, o): the (s, r, o) order re-sorted by relation.
-  counting_sort(rel, n_relations, by_subj, by_rel, &off_rel);
+  sort_by_key(rel, n_relations, by_subj, by_rel, keep_offsets ? &off_rel : nullptr, count);
   // (o, r, s): by object, relation runs inside a row, subjects ascending.
-  counting_sort(subj, n_entities, ident, t1, nullptr);
-  counting_sort(rel, n_relations, t1, t2, nullptr);
-  counting_sort(obj, n_entities, t2, by_obj, &off_obj);
+  sort_by_key(subj, n_entities, ident, t1, nullptr, count);
+  sort_by_key(rel, n_relations, t1, t2, nullptr, count);
+  sort_by_key(obj, n_entities, t2, by_obj, keep_offsets ? &off_obj : nullptr, count);
   std::vector<int32_t>().swap(ident);
   std::vector<int32_t>().swap(t1);
   std::vector<int32_t>().swap(t2);
+  std::vector<int32_t>().swap(count);
   // col_a is gathered for every triple, col_b once per run of equal col_b.
-  fill_layout(out[BY_OBJ], n_entities, std::move(by_obj), std::move(off_obj), subj, rel, weight,
-              keep_perm);
-  fill_layout(out[BY_SUBJ], n_entities, std::move(by_subj), std::move(off_subj), obj, rel,
+  fill_layout(out[BY_OBJ], n_entities, std::move(by_obj), std::move(off_obj), obj, subj, rel,
               weight, keep_perm);
-  fill_layout(out[BY_REL], n_relations, std::move(by_rel), std::move(off_rel), obj, subj, weight,
-              keep_perm);
+  fill_layout(out[BY_SUBJ], n_entities, std::move(by_subj), std::move(off_subj), subj, obj, rel,
+              weight, keep_perm);
+  fill_layout(out[BY_REL], n_relations, std::move(by_rel), std::move(off_rel), rel, obj, subj,
+              weight, keep_perm);
+}
+
+// Rows [first, first + count) as pieces of at most kEmptyPiece rows.
+static void add_empty(PlanHost &P, int64_t first, int64_t count) {
+  P.n_empty_rows += count;
+  for (int64_t q = first; q < first + count; q += kEmptyPiece)
+    P.empty.push_back({(int32_t)q, (int32_t)std::min<int64_t>(kEmptyPiece, first + count - q)});
 }
 
 PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
@@ -104,8 +136,10 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
   P.chunk = chunk;
   P.fan_in = fan_in;
   const bool weighted = !L.weight.empty();
+  const int64_t n_t = (int64_t)L.col_a.size();
   std::vector<Entry> &S = P.entries;
-  S.reserve(L.col_a.size() + L.rows + L.col_a.size() / std::max(1, chunk - 1) + 2);
+  // Triples, at most one marker per triple, chunk-end markers, padding.
+  S.reserve(2 * n_t + n_t / std::max(1, chunk - 1) + chunk + 2);
   if (weighted) P.weights.reserve(S.capacity());
   auto marker = [&](int32_t target) {
     S.push_back({kMarker, target});
@@ -116,13 +150,15 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
     int64_t first, n;
   };
   std::vector<Split> splits;
-  for (int64_t q = 0; q < L.rows; ++q) {
-    const int64_t beg = L.offsets[q], end = L.offsets[q + 1];
+  // The triples come sorted by row; the rows between two rows with triples
+  // (and before the first, after the last) are empty.
+  int64_t next_row = 0;
+  for (int64_t beg = 0, end; beg < n_t; beg = end) {
+    const int64_t q = L.row[beg];
+    for (end = beg + 1; end < n_t && L.row[end] == q;) ++end;
+    add_empty(P, next_row, q - next_row);
+    next_row = q + 1;
     P.max_row_len = std::max(P.max_row_len, end - beg);
-    if (end == beg) {
-      P.empty_rows.push_back((int32_t)q);
-      continue;
-    }
     int64_t first_slot = -1, n_slots = 0;
     bool pending = false;  // triples of this row since the last marker
     for (int64_t p = beg; p < end; ++p) {
@@ -154,6 +190,7 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
       marker((int32_t)q);
     }
   }
+  add_empty(P, next_row, L.rows - next_row);
   // Pad with no-op markers to whole chunks: every lane group then walks
   // exactly `chunk` entries.
   while ((int64_t)S.size() % chunk != 0) marker(kNoTarget);

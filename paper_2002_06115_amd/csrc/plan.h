@@ -28,7 +28,8 @@ struct CombineTask {
 
 struct LayoutHost {
   int64_t rows = 0;
-  std::vector<int32_t> offsets;   // rows + 1
+  std::vector<int32_t> row;       // row id of every position (non-decreasing)
+  std::vector<int32_t> offsets;   // rows + 1 boundaries, only when asked for (O(rows))
   std::vector<int32_t> col_a;     // id of the operand gathered for every triple (A)
   std::vector<int32_t> col_b;     // id of the operand read once per run (B)
   std::vector<float> weight;      // per position, empty for a hard KB
@@ -60,13 +61,21 @@ constexpr int32_t kNoTarget = INT32_MIN;
 // most `fan_in` slots per task, over as many levels as the row needs.
 // Inside a row the triples form runs of equal col_b; the kernel reads a run's
 // B row once, at the entry flagged kRunStart, and keeps it for the run.
+// Rows no triple reaches, as pieces of consecutive rows [first, first + count),
+// count <= kEmptyPiece: one zero-fill task each.
+struct EmptyPiece {
+  int32_t first, count;
+};
+constexpr int32_t kEmptyPiece = 4096;
+
 struct PlanHost {
   int32_t chunk = 0;
   int32_t fan_in = 0;
   int64_t n_chunks = 0;
   std::vector<Entry> entries;
   std::vector<float> weights;       // per entry (markers 0), empty for a hard KB
-  std::vector<int32_t> empty_rows;
+  std::vector<EmptyPiece> empty;    // the rows no triple reaches
+  int64_t n_empty_rows = 0;
   std::vector<std::vector<CombineTask>> levels;
   int64_t n_slots = 0;
   int64_t n_split_rows = 0;
@@ -79,10 +88,12 @@ std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_
                              const int32_t *subj, const int32_t *rel, const int32_t *obj,
                              bool *range_error);
 
-// Builds the three layouts.  keep_perm keeps the caller-index permutation.
+// Builds the three layouts.  keep_perm keeps the caller-index permutation,
+// keep_offsets the per-row boundaries (O(rows); the plans do not need them).
+// Everything else is O(N_T) plus, for dense id spaces, O(N_E + N_R).
 void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                    const int32_t *subj, const int32_t *rel, const int32_t *obj,
-                   const float *weight, bool keep_perm, LayoutHost out[3]);
+                   const float *weight, bool keep_perm, bool keep_offsets, LayoutHost out[3]);
 
 // Cuts a layout into chunks, marks the flush points and plans the combine levels.
 PlanHost plan_layout(const LayoutHost &layout, int32_t chunk, int32_t fan_in);

@@ -1,5 +1,5 @@
 // Host planner under AddressSanitizer and UndefinedBehaviorSanitizer: the
-// validation, the three stable counting sorts and the stream plans of
+// validation, the three stable sorts and the stream plans of
 // random, Zipf-hub, empty and degenerate KBs, with the plan's invariants
 // checked along the way.  Exit status 0 when every check holds (sanitizer
 // reports abort the program).  Built and run by tests/test_host_sanitizers.py.
@@ -50,9 +50,23 @@ static void check_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk, co
   CHECK(triples == (int64_t)L.col_a.size(), "%s: %lld of %zu triples in the stream", what,
         (long long)triples, L.col_a.size());
   int64_t non_empty = 0;
-  for (int64_t q = 0; q < L.rows; ++q) non_empty += L.offsets[q + 1] > L.offsets[q];
+  for (size_t p = 0; p < L.row.size(); ++p) non_empty += p == 0 || L.row[p] != L.row[p - 1];
   CHECK(row_markers + P.n_split_rows == non_empty, "%s: row markers", what);
-  CHECK((int64_t)P.empty_rows.size() == L.rows - non_empty, "%s: empty rows", what);
+  CHECK(P.n_empty_rows == L.rows - non_empty, "%s: empty rows", what);
+  // The empty pieces cover exactly the rows without triples, in order.
+  std::vector<char> has(L.rows, 0);
+  for (int32_t q : L.row) has[q] = 1;
+  int64_t covered = 0, last_end = 0;
+  for (const EmptyPiece &e : P.empty) {
+    CHECK(e.count >= 1 && e.count <= kEmptyPiece && e.first >= last_end &&
+              (int64_t)e.first + e.count <= L.rows,
+          "%s: empty piece (%d, %d)", what, e.first, e.count);
+    for (int32_t q = e.first; q < e.first + e.count && q < L.rows; ++q)
+      CHECK(!has[q], "%s: row %d has triples but is in an empty piece", what, q);
+    covered += e.count;
+    last_end = (int64_t)e.first + e.count;
+  }
+  CHECK(covered == P.n_empty_rows, "%s: empty pieces cover %lld rows", what, (long long)covered);
   // Every stream slot is written once; combine outputs are later slots.
   int64_t stream_slots = 0;
   for (int64_t s = 0; s < P.n_slots; ++s) {
@@ -76,13 +90,18 @@ static void check_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk, co
 }
 
 static void check_layout(const LayoutHost &L, int64_t n_t, const char *what) {
-  CHECK((int64_t)L.col_a.size() == n_t && (int64_t)L.col_b.size() == n_t, "%s: sizes", what);
+  CHECK((int64_t)L.col_a.size() == n_t && (int64_t)L.col_b.size() == n_t &&
+            (int64_t)L.row.size() == n_t,
+        "%s: sizes", what);
   CHECK((int64_t)L.offsets.size() == L.rows + 1 && L.offsets[0] == 0 && L.offsets[L.rows] == n_t,
         "%s: offsets", what);
   for (int64_t q = 0; q < L.rows; ++q) {
     CHECK(L.offsets[q] <= L.offsets[q + 1], "%s: offsets not monotone", what);
-    for (int32_t p = L.offsets[q] + 1; p < L.offsets[q + 1]; ++p)
-      CHECK(L.col_b[p - 1] <= L.col_b[p], "%s: runs not sorted in row %lld", what, (long long)q);
+    for (int32_t p = L.offsets[q]; p < L.offsets[q + 1]; ++p) {
+      CHECK(L.row[p] == q, "%s: row id of position %d", what, p);
+      if (p > L.offsets[q])
+        CHECK(L.col_b[p - 1] <= L.col_b[p], "%s: runs not sorted in row %lld", what, (long long)q);
+    }
   }
 }
 
@@ -98,7 +117,8 @@ static void run_case(const char *what, int64_t n_e, int64_t n_r, std::vector<int
     for (int64_t l = 0; l < n_t; ++l) w[l] = 0.5f + (float)(l % 7);
   }
   LayoutHost L[3];
-  build_layouts(n_e, n_r, n_t, s.data(), r.data(), o.data(), weighted ? w.data() : nullptr, true, L);
+  build_layouts(n_e, n_r, n_t, s.data(), r.data(), o.data(), weighted ? w.data() : nullptr, true,
+                true, L);
   for (int k = 0; k < 3; ++k) {
     check_layout(L[k], n_t, what);
     for (int32_t chunk : {16, 24, 256}) {
@@ -143,6 +163,18 @@ int main() {
       o[l] = (int32_t)(l % 5);
     }
     run_case("hub", 10, 2, s, r, o, true);
+  }
+  // Sparse id space: few triples over many ids (the comparison-sort path).
+  {
+    const int64_t n_e = 1 << 20, n_t = 3000;
+    std::uniform_int_distribution<int32_t> E(0, (int32_t)n_e - 1);
+    std::vector<int32_t> s(n_t), r(n_t), o(n_t);
+    for (int64_t l = 0; l < n_t; ++l) {
+      s[l] = l % 3 ? E(g) : (int32_t)(n_e - 1 - l % 5);
+      r[l] = (int32_t)(l % 4);
+      o[l] = l % 2 ? E(g) : (int32_t)(l % 7);
+    }
+    run_case("sparse ids", n_e, 4, s, r, o, true);
   }
   // Empty KB; one entity with self-loops; one relation.
   run_case("empty", 7, 3, {}, {}, {}, false);

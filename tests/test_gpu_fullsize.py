@@ -99,3 +99,49 @@ def test_large_fullsize_soft_kb(kbf):
 def test_train_fullsize(kbf, integer):
     run_workload(kbf, kbgen.TRAIN, integer)
 
+
+
+def test_maximum_entity_ids(kbf):
+    """N_E = 2^30, the largest id space the library takes, at b = 1 (4 GB per
+    activation; tables of 4 GB or more take the plain-load path): triples at
+    both ends of the id range, integer inputs, every row with a triple and a
+    sample of empty rows checked bit for bit against the oracle."""
+    import torch
+    n_e, n_r, b = 1 << 30, 3, 1
+    g = np.random.default_rng(30)
+    n_t = 4000
+    top = g.integers(n_e - 64, n_e, n_t // 2)
+    low = g.integers(0, 64, n_t // 4)
+    mid = g.integers(0, n_e, n_t - n_t // 2 - n_t // 4)
+    s = np.concatenate([top, low, mid]).astype(np.int32)
+    o = np.concatenate([low, mid, top]).astype(np.int32)
+    r = g.integers(0, n_r, n_t).astype(np.int32)
+    print("[maxsize] kb_create", flush=True)
+    gkb = kbf.KB(s, r, o, n_e, n_r)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(30)
+    X = torch.randint(0, 4, (n_e, b), device="cuda", generator=gen).float()
+    dY = torch.randint(-2, 3, (n_e, b), device="cuda", generator=gen).float()
+    R = torch.tensor([[1.0], [2.0], [-1.0]], device="cuda")
+    print("[maxsize] GPU passes", flush=True)
+    Y = gkb.follow(X, R)
+    dX, dR = gkb.follow_backward(X, R, dY)
+    torch.cuda.synchronize()
+    print("[maxsize] oracle", flush=True)
+    Xh, dYh, Rh = (t.t().contiguous().cpu().numpy() for t in (X, dY, R))
+    empty = np.setdiff1d(np.array([0, 1, 63, 64, n_e // 2, n_e - 65, n_e - 1], np.int64),
+                         np.concatenate([s, o]))
+    rand = g.integers(0, n_e, 32)
+    objs = np.unique(np.concatenate([o, empty, rand])).astype(np.int32)
+    subs = np.unique(np.concatenate([s, empty, rand])).astype(np.int32)
+    rels = np.arange(n_r, dtype=np.int32)
+    args = (s, r, o, n_e, n_r)
+    want_y = oracle.sampled(oracle.SAMPLE_Y, *args, objs, X=Xh, R=Rh)
+    want_dx = oracle.sampled(oracle.SAMPLE_DX, *args, subs, R=Rh, dY=dYh)
+    want_dr = oracle.sampled(oracle.SAMPLE_DR, *args, rels, X=Xh, dY=dYh)
+    idx = lambda t, ids: t[torch.from_numpy(ids.astype(np.int64)).cuda()].t().contiguous().cpu().numpy()
+    assert_bitexact(idx(Y, objs), want_y, "max ids Y")
+    assert_bitexact(idx(dX, subs), want_dx, "max ids dX")
+    assert_bitexact(idx(dR, rels), want_dr, "max ids dR")
+    assert gkb.info()["n_empty_rows"][0] == n_e - len(np.unique(o))
+    gkb.close()
