@@ -86,6 +86,8 @@ def _load_library():
     lib.kb_profile_enable.restype = ctypes.c_int
     lib.kb_profile_read.argtypes = [p, p, p]
     lib.kb_profile_read.restype = ctypes.c_int
+    lib.kb_checked_violations.argtypes = [ctypes.POINTER(ctypes.c_uint64), i32]
+    lib.kb_checked_violations.restype = ctypes.c_int
     return lib
 
 
@@ -107,6 +109,15 @@ def _host_ids(a, n):
 
 def _np_ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def checked_violations(reset=False):
+    """Index violations a checked build (KBFOLLOW_CHECKED) has counted on the
+    current device; raises KBError (KB_ENOTSUP) for a normal build."""
+    count = ctypes.c_uint64()
+    _check(_lib.kb_checked_violations(ctypes.byref(count), 1 if reset else 0),
+           "kb_checked_violations")
+    return int(count.value)
 
 
 def layout_host(subj, rel, obj, n_entities, n_relations, which):

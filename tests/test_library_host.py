@@ -42,10 +42,10 @@ def test_library_exports_every_declared_symbol(kbf):
 
 def test_normal_build_has_no_bounds_checks(kbf):
     count = ctypes.c_uint64(7)
-    lib = kbf._lib
-    lib.kb_checked_violations.argtypes = [ctypes.POINTER(ctypes.c_uint64), ctypes.c_int32]
-    assert lib.kb_checked_violations(ctypes.byref(count), 0) == kbf.KB_ENOTSUP
+    assert kbf._lib.kb_checked_violations(ctypes.byref(count), 0) == kbf.KB_ENOTSUP
     assert count.value == 0
+    with pytest.raises(kbf.KBError):
+        kbf.checked_violations()
 
 
 def test_checked_build_exports_every_declared_symbol():
