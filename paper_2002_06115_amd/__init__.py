@@ -177,16 +177,21 @@ class KB:
     def workspace_size(self, b):
         return int(_lib.kb_workspace_size(self._handle, int(b)))
 
-    def workspace(self, b):
-        """A cached device workspace for batch size b (uint8 tensor or None)."""
+    def workspace(self, b, stream=None):
+        """A cached device workspace for batch size b on `stream` (uint8 tensor
+        or None).  Each stream gets its own, so calls on different streams can
+        run at the same time (calls on one stream are ordered by it)."""
         import torch
         n = self.workspace_size(b)
         if n == 0:
             return None
-        ws = self._ws.get(b)
+        s = torch.cuda.current_stream(self.device) if stream is None else stream
+        key = (b, s.cuda_stream)
+        ws = self._ws.get(key)
         if ws is None or ws.numel() < n:
-            ws = torch.empty(n, dtype=torch.uint8, device=self.device)
-            self._ws[b] = ws
+            with torch.cuda.stream(s):
+                ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+            self._ws[key] = ws
         return ws
 
     def _act(self, t, rows, name):
@@ -217,8 +222,8 @@ class KB:
         if R.shape[1] != b:
             raise ValueError("X and R must have the same batch size")
         Y = torch.empty_like(X) if out is None else self._act(out, self.n_entities, "out")
-        ws = self.workspace(b)
         s = torch.cuda.current_stream(self.device) if stream is None else stream
+        ws = self.workspace(b, s)
         nws = 0 if ws is None else ws.numel()
         with torch.cuda.device(self.device):
             if residual is None:
@@ -250,8 +255,8 @@ class KB:
             dR = torch.empty((self.n_relations, b), dtype=torch.float32, device=self.device)
         dX = self._act(dX, self.n_entities, "dX") if want_dx else None
         dR = self._act(dR, self.n_relations, "dR") if want_dr else None
-        ws = self.workspace(b)
         s = torch.cuda.current_stream(self.device) if stream is None else stream
+        ws = self.workspace(b, s)
         nws = 0 if ws is None else ws.numel()
         with torch.cuda.device(self.device):
             if residual is None:
