@@ -37,23 +37,41 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def pass_bytes(kb, b, phase):
-    """Algorithmic bytes of one stream-kernel launch (gather model: every
-    triple's b-wide operand rows come from memory; plus the index stream and
-    the output rows), and the compulsory model (each distinct row once)."""
+_DISTINCT = {}
+
+
+def distinct_ids(kb):
+    """Number of distinct subjects and of distinct objects of the KB."""
+    key = id(kb)
+    if key not in _DISTINCT:
+        _DISTINCT[key] = (len(np.unique(kb.subj)), len(np.unique(kb.obj)))
+    return _DISTINCT[key]
+
+
+def pass_bytes(kb, b, phase, whole_pass=False):
+    """Algorithmic bytes of one stream-kernel launch under three models, all
+    with the index stream (8 B per triple), the row offsets and R:
+      gather      every triple's b-wide operand rows come from memory;
+      compulsory  each distinct gathered row once (rows no triple names are
+                  never read);
+      array_once  each operand array read once in full.
+    The stream kernel writes the output rows that have triples; with
+    whole_pass the rows without triples (written by the zero fill) count
+    too, as for the whole pass."""
     n_t, n_e, n_r = kb.n_triples, kb.n_entities, kb.n_relations
     idx = 8 * n_t
+    n_subj, n_obj = distinct_ids(kb)
     if phase in ("fwd_stream", "dx_stream"):
-        gather = idx + 4 * (n_e + 1) + 4 * b * n_t + 4 * b * n_e      # A gathered per triple, R from LDS/L2
-        a_ids = kb.subj if phase == "fwd_stream" else kb.obj
-        out_ids = kb.obj if phase == "fwd_stream" else kb.subj
-        comp = idx + 4 * (n_e + 1) + 4 * b * len(np.unique(a_ids)) + 4 * b * n_r \
-            + 4 * b * len(np.unique(out_ids))
+        n_a, n_out = (n_subj, n_obj) if phase == "fwd_stream" else (n_obj, n_subj)
+        out = 4 * b * (n_e if whole_pass else n_out)
+        gather = idx + 4 * (n_e + 1) + 4 * b * n_t + 4 * b * n_r + out    # A gathered per triple
+        comp = idx + 4 * (n_e + 1) + 4 * b * n_a + 4 * b * n_r + out
+        once = idx + 4 * (n_e + 1) + 4 * b * n_e + 4 * b * n_r + out
     else:
         gather = idx + 4 * (n_r + 1) + 8 * b * n_t + 4 * b * n_r
-        comp = idx + 4 * (n_r + 1) + 4 * b * (len(np.unique(kb.subj)) + len(np.unique(kb.obj))) \
-            + 4 * b * n_r
-    return float(gather), float(comp)
+        comp = idx + 4 * (n_r + 1) + 4 * b * (n_subj + n_obj) + 4 * b * n_r
+        once = idx + 4 * (n_r + 1) + 8 * b * n_e + 4 * b * n_r
+    return float(gather), float(comp), float(once)
 
 
 def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False):
@@ -202,17 +220,19 @@ def probe_lib():
     lib.kbp_gather_time.argtypes = [P, I64, I32, P, I32, P, I32, P, F]
     lib.kbp_stream_read_time.argtypes = [P, I64, I32, P, I32, P, F]
     lib.kbp_stream_copy_time.argtypes = [P, P, I64, I32, I32, P, F]
+    lib.kbp_stream_write_time.argtypes = [P, I64, I32, I32, P, F]
     return lib
 
 
 def stream_rates(torch, lib, reps=10):
     """Device streaming rates on a 2 GiB buffer (best over a few grid sizes):
-    sequential read GB/s and copy GB/s (bytes read + written)."""
+    sequential read GB/s, copy GB/s (bytes read + written) and non-temporal
+    zero-fill GB/s."""
     import ctypes
     n = (2 << 30) // 4
     src = torch.ones(n, device="cuda")
     dst = torch.empty_like(src)
-    read, copy = [], []
+    read, copy, write = [], [], []
     for blocks in (1024, 4096, 16384):
         scratch = torch.empty(blocks * 256, device="cuda")
         ms = ctypes.c_float()
@@ -224,8 +244,12 @@ def stream_rates(torch, lib, reps=10):
                                     ctypes.byref(ms)) != 0:
             raise SystemExit("kbp_stream_copy_time failed")
         copy.append(2 * 4 * n / (ms.value * 1e-3) / 1e9)
+        if lib.kbp_stream_write_time(dst.data_ptr(), n // 4, blocks, reps, None,
+                                     ctypes.byref(ms)) != 0:
+            raise SystemExit("kbp_stream_write_time failed")
+        write.append(4 * n / (ms.value * 1e-3) / 1e9)
     del src, dst, scratch
-    return round(max(read), 1), round(max(copy), 1)
+    return round(max(read), 1), round(max(copy), 1), round(max(write), 1)
 
 
 def gather_probe(args, torch, kbgen, kbf):
@@ -256,8 +280,9 @@ def gather_probe(args, torch, kbgen, kbf):
     gkb.profile(False)
     passes = {k: round(ph[k][0] / max(1, ph[k][1]), 4) for k in ("fwd_stream", "dx_stream",
                                                                   "dr_stream")}
-    stream_read, stream_copy = stream_rates(torch, lib)
-    log(f"[probe] 2 GiB sequential read {stream_read} GB/s, copy {stream_copy} GB/s")
+    stream_read, stream_copy, stream_write = stream_rates(torch, lib)
+    log(f"[probe] 2 GiB sequential read {stream_read} GB/s, copy {stream_copy} GB/s, "
+        f"zero fill {stream_write} GB/s")
     lay = {which: kbf.layout_host(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations, which)
            for which in (0, 1, 2)}
     rng = np.random.default_rng(np.random.SeedSequence([20020615, 99]))
@@ -448,14 +473,15 @@ def main():
             iters)
         lib = probe_lib()
         if lib is not None:
-            detail["stream_read_GBps"], detail["copy_GBps"] = stream_rates(torch, lib)
+            (detail["stream_read_GBps"], detail["copy_GBps"],
+             detail["write_GBps"]) = stream_rates(torch, lib)
         log(f"[bench] detail {json.dumps(detail)}")
 
     roof = None
     if phases:
         dom = max(("fwd_stream", "dx_stream", "dr_stream"), key=lambda p: phases[p][0])
         ms_avg = phases[dom][0] / max(1, phases[dom][1])
-        gather_b, comp_b = pass_bytes(kb, b, dom)
+        gather_b, comp_b, once_b = pass_bytes(kb, b, dom)
         sec = ms_avg * 1e-3
         symbol = stream_kernel_symbol(b, residual=args.residual is not None,
                                       plain_loads=os.environ.get("KBFOLLOW_PLAIN_LOADS") == "1")
@@ -468,7 +494,20 @@ def main():
                                "gathered row once, R, every output row once",
                 "algorithmic_bytes": comp_b,
                 "gather_model_bytes": gather_b,
-                "gather_model_GBps": round(gather_b / sec / 1e9, 1)}
+                "gather_model_GBps": round(gather_b / sec / 1e9, 1),
+                "array_once_bytes": once_b,
+                "array_once_GBps": round(once_b / sec / 1e9, 1),
+                "array_once_frac": round(once_b / sec / 1e9 / PEAK_HBM_GBPS, 4)}
+        # The whole step (fwd + dX + dR and their combine and zero-fill
+        # launches) against the three passes' bytes.
+        step_sec = ms_step * 1e-3
+        step = [pass_bytes(kb, b, p, whole_pass=True) for p in ("fwd_stream", "dx_stream", "dr_stream")]
+        step_comp, step_once = sum(x[1] for x in step), sum(x[2] for x in step)
+        roof["step"] = {"ms": round(ms_step, 4),
+                        "compulsory_bytes": step_comp,
+                        "compulsory_frac": round(step_comp / step_sec / 1e9 / PEAK_HBM_GBPS, 4),
+                        "array_once_bytes": step_once,
+                        "array_once_frac": round(step_once / step_sec / 1e9 / PEAK_HBM_GBPS, 4)}
         if traffic:
             roof["hbm_measured_GBps"] = round(traffic / sec / 1e9, 1)
             roof["hbm_measured_frac"] = round(traffic / sec / 1e9 / PEAK_HBM_GBPS, 4)

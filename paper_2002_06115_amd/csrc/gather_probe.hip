@@ -89,6 +89,15 @@ __global__ __launch_bounds__(kBlock) void stream_copy_kernel(const native_float4
     __builtin_nontemporal_store(__builtin_nontemporal_load(X + i), Y + i);
 }
 
+// Fill of n float4s with zeros, grid-stride, non-temporal stores.
+__global__ __launch_bounds__(kBlock) void stream_write_kernel(int64_t n,
+                                                              native_float4 *__restrict__ Y) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const native_float4 z = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
+    __builtin_nontemporal_store(z, Y + i);
+}
+
 // One untimed launch, then `reps` launches between two events on `s`;
 // *ms = mean time of one.  0 on success, -2 on a HIP error.
 template <class Run>
@@ -147,6 +156,21 @@ int kbp_stream_copy_time(const void *X, void *Y, int64_t n_float4, int32_t n_blo
     hipLaunchKernelGGL(stream_copy_kernel, dim3((unsigned)n_blocks), dim3(kBlock), 0, s,
                        static_cast<const native_float4 *>(X), n_float4,
                        static_cast<native_float4 *>(Y));
+  };
+  return time_launches(run, reps, s, ms);
+}
+
+// Writes zeros over n_float4 float4s of DEVICE Y, front to back, `reps`
+// timed launches after one untimed; *ms receives the mean time of one.
+// n_blocks >= 1 workgroups of 256.  Returns 0, -1 for bad arguments, -2 for
+// a HIP error.
+int kbp_stream_write_time(void *Y, int64_t n_float4, int32_t n_blocks, int32_t reps, void *stream,
+                          float *ms) {
+  if (!Y || !ms || n_float4 < 1 || n_blocks < 1 || reps < 1) return -1;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto run = [&]() {
+    hipLaunchKernelGGL(stream_write_kernel, dim3((unsigned)n_blocks), dim3(kBlock), 0, s,
+                       n_float4, static_cast<native_float4 *>(Y));
   };
   return time_launches(run, reps, s, ms);
 }

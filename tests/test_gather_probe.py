@@ -31,6 +31,7 @@ def test_probe_library_exports_entry_points():
     assert hasattr(lib, "kbp_gather_time")
     assert hasattr(lib, "kbp_stream_read_time")
     assert hasattr(lib, "kbp_stream_copy_time")
+    assert hasattr(lib, "kbp_stream_write_time")
 
 
 def _copy_lib():
@@ -47,6 +48,22 @@ def test_stream_copy_rejects_bad_arguments(n4, blocks, reps):
     ms = ctypes.c_float()
     assert _copy_lib().kbp_stream_copy_time(dummy, dummy, n4, blocks, reps, None,
                                             ctypes.byref(ms)) == -1
+
+
+def _write_lib():
+    lib = ctypes.CDLL(PROBE)
+    lib.kbp_stream_write_time.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                          ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.POINTER(ctypes.c_float)]
+    return lib
+
+
+@pytest.mark.parametrize("n4,blocks,reps", [(0, 4, 1), (16, 0, 1), (16, 4, 0)])
+def test_stream_write_rejects_bad_arguments(n4, blocks, reps):
+    dummy = ctypes.c_void_p(16)  # never dereferenced: arguments are checked first
+    ms = ctypes.c_float()
+    assert _write_lib().kbp_stream_write_time(dummy, n4, blocks, reps, None,
+                                              ctypes.byref(ms)) == -1
 
 
 @pytest.mark.parametrize("n4,blocks,reps", [(0, 4, 1), (16, 0, 1), (16, 4, 0)])
@@ -101,3 +118,17 @@ def test_stream_copy_copies():
     assert _copy_lib().kbp_stream_copy_time(src.data_ptr(), dst.data_ptr(), 5000, 7, 2, None,
                                             ctypes.byref(ms)) == 0
     assert torch.equal(src, dst) and ms.value > 0
+
+
+@pytest.mark.gpu
+def test_stream_write_zero_fills():
+    import torch
+    dst = torch.full((4 * 5003,), float("nan"), device="cuda")
+    guard = torch.full((64,), 7.0, device="cuda")
+    ms = ctypes.c_float()
+    assert _write_lib().kbp_stream_write_time(dst.data_ptr(), 5000, 7, 2, None,
+                                              ctypes.byref(ms)) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:20000], torch.zeros(20000, device="cuda")) and ms.value > 0
+    assert torch.isnan(dst[20000:]).all()  # only n_float4 float4s written
+    assert torch.equal(guard, torch.full((64,), 7.0, device="cuda"))
