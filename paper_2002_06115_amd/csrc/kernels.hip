@@ -398,9 +398,13 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
   }
 }
 
-// Writes the rows no triple reaches: one lane group per piece of consecutive
-// rows (first, count), lanes over the columns as in the stream kernel.
-template <int VEC, int LPT>
+// Writes the rows no triple reaches, given as pieces of consecutive rows
+// (first, count); lanes over the columns as in the stream kernel.  PACKED: a
+// lane group writes LPT consecutive pieces, whose descriptors its lanes fetch
+// with one load (lane j the j-th) and share by shuffles, so that one load
+// stands in front of the stores of 64 pieces per wave.  Otherwise one piece
+// per group: the residual hop's rows each need a load of X of their own.
+template <int VEC, int LPT, bool PACKED>
 __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int2 *__restrict__ pieces,
                                                            int64_t n_pieces, int32_t b,
                                                            float *__restrict__ out,
@@ -412,26 +416,37 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int2 *__restric
   const int lane = threadIdx.x % LPT;
   const int grp = threadIdx.x / LPT;
   const int c = blockIdx.y * W + lane * VEC;
-  if (c >= b) return;  // no barrier below
   const size_t bb = (size_t)b;
-  const int64_t stride = (int64_t)gridDim.x * GPB;
-  for (int64_t t = (int64_t)blockIdx.x * GPB + grp; t < n_pieces; t += stride) {
-    const int2 pc = pieces[t];  // first row, count
-    for (int i = 0; i < pc.y; ++i) {
-      const size_t off = (size_t)KBF_CHECKED((int64_t)pc.x + i, out_rows) * bb + c;
-      double y[VEC];
-      if (res) {
-        float r[VEC];
-        load_row<VEC>(res + off, r);
+  if constexpr (PACKED) {
+    const int64_t t = ((int64_t)blockIdx.x * GPB + grp) * LPT + lane;
+    int2 mine = make_int2(0, 0);  // past the end: a piece of no rows
+    if (t < n_pieces) mine = pieces[t];
+    const int base = (int)(threadIdx.x % 64) - lane;  // lane 0 of this group in the wave
+    for (int j = 0; j < LPT; ++j) {
+      const int first = __shfl(mine.x, base + j);
+      const int count = __shfl(mine.y, base + j);
+      if (c >= b) continue;  // after the shuffles, which every lane joins
+      for (int i = 0; i < count; ++i) {
+        const double z[VEC] = {};
+        // Non-temporal, like every output row: plain stores would leave the
+        // rows dirty in the caches, to be written back during the next pass.
+        store_row<VEC>(out + (size_t)KBF_CHECKED((int64_t)first + i, out_rows) * bb + c, z);
+      }
+    }
+  } else {
+    if (c >= b) return;  // no barrier or shuffle below
+    const int64_t stride = (int64_t)gridDim.x * GPB;
+    for (int64_t t = (int64_t)blockIdx.x * GPB + grp; t < n_pieces; t += stride) {
+      const int2 pc = pieces[t];  // first row, count
+      for (int i = 0; i < pc.y; ++i) {
+        const size_t off = (size_t)KBF_CHECKED((int64_t)pc.x + i, out_rows) * bb + c;
+        double y[VEC];
+        float r[VEC] = {};
+        if (res) load_row<VEC>(res + off, r);
 #pragma unroll
         for (int v = 0; v < VEC; ++v) y[v] = 0.0 + (double)gamma * (double)r[v];
-      } else {
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) y[v] = 0.0;
+        store_row<VEC>(out + off, y);
       }
-      // Non-temporal, like every output row: plain stores would leave the
-      // rows dirty in the caches, to be written back during the next pass.
-      store_row<VEC>(out + off, y);
     }
   }
 }
@@ -476,16 +491,16 @@ const void *combine_fn(int lpt) {
   return nullptr;
 }
 
-template <int VEC>
+template <int VEC, bool PACKED>
 const void *zero_fn(int lpt) {
   switch (lpt) {
-    case 1: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 1>);
-    case 2: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 2>);
-    case 4: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 4>);
-    case 8: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 8>);
-    case 16: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 16>);
-    case 32: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 32>);
-    case 64: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 64>);
+    case 1: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 1, PACKED>);
+    case 2: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 2, PACKED>);
+    case 4: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 4, PACKED>);
+    case 8: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 8, PACKED>);
+    case 16: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 16, PACKED>);
+    case 32: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 32, PACKED>);
+    case 64: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 64, PACKED>);
   }
   return nullptr;
 }
@@ -546,11 +561,15 @@ hipError_t launch_zero_rows(const int2 *pieces, int64_t n_pieces, int32_t b, flo
                             int64_t out_rows, const float *res, float gamma, hipStream_t s) {
   if (n_pieces == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(b);
-  const void *fn = t.vec == 4 ? zero_fn<4>(t.lpt) : zero_fn<1>(t.lpt);
+  const bool packed = res == nullptr;
+  const void *fn = t.vec == 4 ? (packed ? zero_fn<4, true>(t.lpt) : zero_fn<4, false>(t.lpt))
+                              : (packed ? zero_fn<1, true>(t.lpt) : zero_fn<1, false>(t.lpt));
   if (!fn) return hipErrorInvalidValue;
-  // One piece per lane group: each piece's row range is then the only load
-  // in front of its stores.
-  const dim3 grid((unsigned)blocks_for(n_pieces, kBlock / t.lpt, 0), (unsigned)t.n_slices);
+  // Packed: LPT pieces per lane group, 256 per block.  Residual: one piece
+  // per lane group, so that each piece's rows are the only loads in front of
+  // their stores.
+  const int per_block = packed ? kBlock : kBlock / t.lpt;
+  const dim3 grid((unsigned)blocks_for(n_pieces, per_block, 0), (unsigned)t.n_slices);
   void *params[] = {&pieces, &n_pieces, &b, &out, &out_rows, &res, &gamma};
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
