@@ -215,11 +215,14 @@ kb_status kb_checked_violations(uint64_t *count, int32_t reset);
  * Kernel timing with HIP events (for benchmarks; not thread safe)
  * ------------------------------------------------------------------------ */
 
-/* Phases whose GPU time is recorded when profiling is on. */
+/* Phases whose GPU time is recorded when profiling is on.  Per pass: STREAM
+ * is the stream kernel; TAIL the one launch that does the first combine
+ * level (rows split over several chunks) and writes the rows without
+ * triples; COMBINE the further combine levels (rows split over many chunks). */
 typedef enum {
-  KB_PH_FWD_STREAM = 0, KB_PH_FWD_COMBINE, KB_PH_FWD_ZERO,
-  KB_PH_DX_STREAM, KB_PH_DX_COMBINE, KB_PH_DX_ZERO,
-  KB_PH_DR_STREAM, KB_PH_DR_COMBINE, KB_PH_DR_ZERO,
+  KB_PH_FWD_STREAM = 0, KB_PH_FWD_TAIL, KB_PH_FWD_COMBINE,
+  KB_PH_DX_STREAM, KB_PH_DX_TAIL, KB_PH_DX_COMBINE,
+  KB_PH_DR_STREAM, KB_PH_DR_TAIL, KB_PH_DR_COMBINE,
   KB_PH_COUNT
 } kb_phase;
 

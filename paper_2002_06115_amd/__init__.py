@@ -27,8 +27,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("KBFOLLOW_LIB") or os.path.join(_PKG, "_lib", "libkbfollow.so")
 
 KB_OK, KB_EINVAL, KB_ERANGE, KB_ENOMEM, KB_EHIP, KB_ENOTSUP = range(6)
-PHASES = ("fwd_stream", "fwd_combine", "fwd_zero", "dx_stream", "dx_combine", "dx_zero",
-          "dr_stream", "dr_combine", "dr_zero")
+PHASES = ("fwd_stream", "fwd_tail", "fwd_combine", "dx_stream", "dx_tail", "dx_combine",
+          "dr_stream", "dr_tail", "dr_combine")
 
 
 class KBError(RuntimeError):

@@ -199,7 +199,8 @@ kb_status check_device(const kb_t *kb) {
   return KB_OK;
 }
 
-// Runs one pass: the stream kernel, the combine levels, the empty rows.  With
+// Runs one pass: the stream kernel, the first combine level together with
+// the empty rows, the further combine levels.  With
 // residual set (A has one row per output row) every output row j also gets
 // gamma * A[j].
 kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float *A,
@@ -215,18 +216,22 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
   {
+    // The first combine level and the empty rows share one launch.
     PhaseScope scope(kb, ph_base + 1, s);
-    for (size_t L = 0; L + 1 < D.level_begin.size(); ++L) {
+    const int64_t n0 = D.level_begin.size() > 1 ? D.level_begin[1] - D.level_begin[0] : 0;
+    TailArgs t{D.ctasks, n0, slots, D.n_slots, D.empty, D.n_empty_pieces, b, out, D.rows, res,
+               gamma, 0};
+    hipError_t e = launch_tail(t, s);
+    if (e != hipSuccess) return hip_fail(e, "combine and empty-row kernel launch");
+  }
+  {
+    PhaseScope scope(kb, ph_base + 2, s);
+    for (size_t L = 1; L + 1 < D.level_begin.size(); ++L) {
       const int64_t n = D.level_begin[L + 1] - D.level_begin[L];
       hipError_t e = launch_combine(D.ctasks + D.level_begin[L], n, slots, D.n_slots, b, out,
                                     D.rows, res, gamma, s);
       if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
     }
-  }
-  {
-    PhaseScope scope(kb, ph_base + 2, s);
-    hipError_t e = launch_zero_rows(D.empty, D.n_empty_pieces, b, out, D.rows, res, gamma, s);
-    if (e != hipSuccess) return hip_fail(e, "zero-rows kernel launch");
   }
   return KB_OK;
 }

@@ -58,10 +58,25 @@ hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int
                           int32_t b, float *out, int64_t out_rows, const float *res, float gamma,
                           hipStream_t s);
 
-// Writes +0.0 to the rows of out ([out_rows][b]) in the given pieces (first
-// row, count), or gamma * res[row] when res is not null (residual hop).
-hipError_t launch_zero_rows(const int2 *pieces, int64_t n_pieces, int32_t b, float *out,
-                            int64_t out_rows, const float *res, float gamma, hipStream_t s);
+// One launch for a pass's first combine level (tasks of that level, as for
+// launch_combine) and its empty rows: +0.0 to the rows of out in the pieces
+// (first row, count), or gamma * res[row] when res is not null (residual
+// hop).  combine_blocks is set by the launcher.
+struct TailArgs {
+  const int4 *tasks;
+  int64_t n_tasks;
+  double *slots;
+  int64_t n_slots;
+  const int2 *pieces;
+  int64_t n_pieces;
+  int32_t b;
+  float *out;
+  int64_t out_rows;
+  const float *res;
+  float gamma;
+  int64_t combine_blocks;
+};
+hipError_t launch_tail(const TailArgs &a, hipStream_t s);
 
 // Bounds violations counted by a checked build (KBFOLLOW_CHECKED) on the
 // current device since the last reset; hipErrorNotSupported otherwise.

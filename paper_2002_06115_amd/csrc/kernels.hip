@@ -347,15 +347,13 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
 }
 
 // Adds slots [first, first + n) in increasing order; writes the float row or
-// a next-level slot.
+// a next-level slot.  `block` of `n_blocks` blocks share the tasks.
 template <int VEC, int LPT>
-__global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict__ tasks,
-                                                         int64_t n_tasks,
-                                                         double *__restrict__ slots,
-                                                         int64_t n_slots, int32_t b,
-                                                         float *__restrict__ out, int64_t out_rows,
-                                                         const float *__restrict__ res,
-                                                         float gamma) {
+__device__ __forceinline__ void combine_tasks(const int4 *__restrict__ tasks, int64_t n_tasks,
+                                              double *__restrict__ slots, int64_t n_slots,
+                                              int32_t b, float *__restrict__ out,
+                                              int64_t out_rows, const float *__restrict__ res,
+                                              float gamma, int64_t block, int64_t n_blocks) {
   constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
   const int lane = threadIdx.x % LPT;
@@ -363,8 +361,8 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
   const int c = blockIdx.y * W + lane * VEC;
   if (c >= b) return;  // no barrier below
   const size_t bb = (size_t)b;
-  const int64_t stride = (int64_t)gridDim.x * GPB;
-  for (int64_t t = (int64_t)blockIdx.x * GPB + grp; t < n_tasks; t += stride) {
+  const int64_t stride = n_blocks * GPB;
+  for (int64_t t = block * GPB + grp; t < n_tasks; t += stride) {
     const int4 tk = tasks[t];  // first, n, dst
     double acc[VEC];
 #pragma unroll
@@ -404,13 +402,12 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
 // with one load (lane j the j-th) and share by shuffles, so that one load
 // stands in front of the stores of 64 pieces per wave.  Otherwise one piece
 // per group: the residual hop's rows each need a load of X of their own.
+// `block` of `n_blocks` blocks share the pieces.
 template <int VEC, int LPT, bool PACKED>
-__global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int2 *__restrict__ pieces,
-                                                           int64_t n_pieces, int32_t b,
-                                                           float *__restrict__ out,
-                                                           int64_t out_rows,
-                                                           const float *__restrict__ res,
-                                                           float gamma) {
+__device__ __forceinline__ void zero_pieces(const int2 *__restrict__ pieces, int64_t n_pieces,
+                                            int32_t b, float *__restrict__ out, int64_t out_rows,
+                                            const float *__restrict__ res, float gamma,
+                                            int64_t block, int64_t n_blocks) {
   constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
   const int lane = threadIdx.x % LPT;
@@ -418,25 +415,29 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int2 *__restric
   const int c = blockIdx.y * W + lane * VEC;
   const size_t bb = (size_t)b;
   if constexpr (PACKED) {
-    const int64_t t = ((int64_t)blockIdx.x * GPB + grp) * LPT + lane;
-    int2 mine = make_int2(0, 0);  // past the end: a piece of no rows
-    if (t < n_pieces) mine = pieces[t];
-    const int base = (int)(threadIdx.x % 64) - lane;  // lane 0 of this group in the wave
-    for (int j = 0; j < LPT; ++j) {
-      const int first = __shfl(mine.x, base + j);
-      const int count = __shfl(mine.y, base + j);
-      if (c >= b) continue;  // after the shuffles, which every lane joins
-      for (int i = 0; i < count; ++i) {
-        const double z[VEC] = {};
-        // Non-temporal, like every output row: plain stores would leave the
-        // rows dirty in the caches, to be written back during the next pass.
-        store_row<VEC>(out + (size_t)KBF_CHECKED((int64_t)first + i, out_rows) * bb + c, z);
+    const int64_t stride = n_blocks * kBlock;
+    for (int64_t t0 = (block * GPB + grp) * LPT; t0 < n_pieces; t0 += stride) {
+      const int64_t t = t0 + lane;
+      int2 mine = make_int2(0, 0);  // past the end: a piece of no rows
+      if (t < n_pieces) mine = pieces[t];
+      const int base = (int)(threadIdx.x % 64) - lane;  // lane 0 of this group in the wave
+      for (int j = 0; j < LPT; ++j) {
+        const int first = __shfl(mine.x, base + j);
+        const int count = __shfl(mine.y, base + j);
+        if (c >= b) continue;  // after the shuffles, which every lane joins
+        for (int i = 0; i < count; ++i) {
+          const double z[VEC] = {};
+          // Non-temporal, like every output row: plain stores would leave
+          // the rows dirty in the caches, to be written back during the next
+          // pass.
+          store_row<VEC>(out + (size_t)KBF_CHECKED((int64_t)first + i, out_rows) * bb + c, z);
+        }
       }
     }
   } else {
     if (c >= b) return;  // no barrier or shuffle below
-    const int64_t stride = (int64_t)gridDim.x * GPB;
-    for (int64_t t = (int64_t)blockIdx.x * GPB + grp; t < n_pieces; t += stride) {
+    const int64_t stride = n_blocks * GPB;
+    for (int64_t t = block * GPB + grp; t < n_pieces; t += stride) {
       const int2 pc = pieces[t];  // first row, count
       for (int i = 0; i < pc.y; ++i) {
         const size_t off = (size_t)KBF_CHECKED((int64_t)pc.x + i, out_rows) * bb + c;
@@ -449,6 +450,34 @@ __global__ __launch_bounds__(kBlock) void zero_rows_kernel(const int2 *__restric
       }
     }
   }
+}
+
+// A later combine level.
+template <int VEC, int LPT>
+__global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict__ tasks,
+                                                         int64_t n_tasks,
+                                                         double *__restrict__ slots,
+                                                         int64_t n_slots, int32_t b,
+                                                         float *__restrict__ out, int64_t out_rows,
+                                                         const float *__restrict__ res,
+                                                         float gamma) {
+  combine_tasks<VEC, LPT>(tasks, n_tasks, slots, n_slots, b, out, out_rows, res, gamma,
+                          blockIdx.x, gridDim.x);
+}
+
+// The first combine level and the empty rows in one launch: blocks
+// [0, combine_blocks) take the combine tasks, the others the empty-row
+// pieces.  The two write disjoint rows; the combine's dependent slot reads
+// overlap with the fill's stores instead of forming a launch of their own.
+template <int VEC, int LPT, bool PACKED>
+__global__ __launch_bounds__(kBlock) void tail_kernel(TailArgs a) {
+  if ((int64_t)blockIdx.x < a.combine_blocks)
+    combine_tasks<VEC, LPT>(a.tasks, a.n_tasks, a.slots, a.n_slots, a.b, a.out, a.out_rows,
+                            a.res, a.gamma, blockIdx.x, a.combine_blocks);
+  else
+    zero_pieces<VEC, LPT, PACKED>(a.pieces, a.n_pieces, a.b, a.out, a.out_rows, a.res, a.gamma,
+                                  (int64_t)blockIdx.x - a.combine_blocks,
+                                  (int64_t)gridDim.x - a.combine_blocks);
 }
 
 template <int VEC, bool BUF, bool WT, bool RES>
@@ -492,15 +521,15 @@ const void *combine_fn(int lpt) {
 }
 
 template <int VEC, bool PACKED>
-const void *zero_fn(int lpt) {
+const void *tail_fn(int lpt) {
   switch (lpt) {
-    case 1: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 1, PACKED>);
-    case 2: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 2, PACKED>);
-    case 4: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 4, PACKED>);
-    case 8: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 8, PACKED>);
-    case 16: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 16, PACKED>);
-    case 32: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 32, PACKED>);
-    case 64: return reinterpret_cast<const void *>(&zero_rows_kernel<VEC, 64, PACKED>);
+    case 1: return reinterpret_cast<const void *>(&tail_kernel<VEC, 1, PACKED>);
+    case 2: return reinterpret_cast<const void *>(&tail_kernel<VEC, 2, PACKED>);
+    case 4: return reinterpret_cast<const void *>(&tail_kernel<VEC, 4, PACKED>);
+    case 8: return reinterpret_cast<const void *>(&tail_kernel<VEC, 8, PACKED>);
+    case 16: return reinterpret_cast<const void *>(&tail_kernel<VEC, 16, PACKED>);
+    case 32: return reinterpret_cast<const void *>(&tail_kernel<VEC, 32, PACKED>);
+    case 64: return reinterpret_cast<const void *>(&tail_kernel<VEC, 64, PACKED>);
   }
   return nullptr;
 }
@@ -557,20 +586,23 @@ hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 
-hipError_t launch_zero_rows(const int2 *pieces, int64_t n_pieces, int32_t b, float *out,
-                            int64_t out_rows, const float *res, float gamma, hipStream_t s) {
-  if (n_pieces == 0) return hipSuccess;
-  const ColumnTiling t = column_tiling(b);
-  const bool packed = res == nullptr;
-  const void *fn = t.vec == 4 ? (packed ? zero_fn<4, true>(t.lpt) : zero_fn<4, false>(t.lpt))
-                              : (packed ? zero_fn<1, true>(t.lpt) : zero_fn<1, false>(t.lpt));
+hipError_t launch_tail(const TailArgs &args, hipStream_t s) {
+  if (args.n_tasks == 0 && args.n_pieces == 0) return hipSuccess;
+  const ColumnTiling t = column_tiling(args.b);
+  const bool packed = args.res == nullptr;
+  const void *fn = t.vec == 4 ? (packed ? tail_fn<4, true>(t.lpt) : tail_fn<4, false>(t.lpt))
+                              : (packed ? tail_fn<1, true>(t.lpt) : tail_fn<1, false>(t.lpt));
   if (!fn) return hipErrorInvalidValue;
-  // Packed: LPT pieces per lane group, 256 per block.  Residual: one piece
-  // per lane group, so that each piece's rows are the only loads in front of
-  // their stores.
-  const int per_block = packed ? kBlock : kBlock / t.lpt;
-  const dim3 grid((unsigned)blocks_for(n_pieces, per_block, 0), (unsigned)t.n_slices);
-  void *params[] = {&pieces, &n_pieces, &b, &out, &out_rows, &res, &gamma};
+  TailArgs a = args;
+  // One combine task per lane group.  Empty rows, packed: LPT pieces per
+  // lane group, 256 per block; residual: one piece per lane group, so that
+  // each piece's rows are the only loads in front of their stores.
+  a.combine_blocks = a.n_tasks > 0 ? blocks_for(a.n_tasks, kBlock / t.lpt, 0) : 0;
+  const int64_t zero_blocks =
+      a.n_pieces > 0 ? blocks_for(a.n_pieces, packed ? kBlock : kBlock / t.lpt, 0) : 0;
+  if (a.combine_blocks + zero_blocks > (int64_t)INT32_MAX) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(a.combine_blocks + zero_blocks), (unsigned)t.n_slices);
+  void *params[] = {&a};
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 
