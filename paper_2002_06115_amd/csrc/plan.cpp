@@ -3,10 +3,11 @@
 // The reified KB of Sec. 2.3 keeps, per triple, its subject, object and
 // relation ids (the one nonzero of row l in M_subj, M_obj and M_rel).  Here
 // the triples are sorted three ways with stable sorts: by (o, r, s), by
-// (s, r, o) and by (r, s, o) -- counting sorts over dense id spaces,
-// comparison sorts where the id space is far larger than the KB -- and the
-// plans are built from the sorted rows alone, so building a KB costs
-// O(N_T + number of empty-row ranges) beyond the counting sorts.  The secondary key
+// (s, r, o) and by (r, s, o) -- a radix sort of one 64-bit key per triple
+// where the three ids fit one, else chained counting sorts over dense id
+// spaces and comparison sorts where the id space is far larger than the KB
+// -- and the plans are built from the sorted rows alone, so building a KB
+// costs O(N_T + number of empty-row ranges) beyond the sorts.  The secondary key
 // groups each row into runs of equal second operand (the relation for the
 // forward and dX passes, the subject for dR), so the kernels read that
 // operand once per run instead of once per triple.
@@ -14,6 +15,8 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <exception>
+#include <thread>
 
 namespace kbf {
 
@@ -94,9 +97,147 @@ static void fill_layout(LayoutHost &L, int64_t rows, std::vector<int32_t> &&orde
   if (keep_perm) L.perm = std::move(order);
 }
 
+// Stable LSD radix sort of `key` (11-bit digits, as many passes as the
+// largest key has digits; all digit histograms from one read), carrying the
+// triple ids along when `id` is non-null.  Each pass is a sequential read and
+// a scatter into 2048 buckets, unlike a counting sort over an id space of
+// millions, whose gathers and scatters miss the caches.
+static void radix_sort(std::vector<uint64_t> &key, std::vector<int32_t> *id) {
+  constexpr int kBits = 11, kDigits = 1 << kBits, kMaxPasses = (64 + kBits - 1) / kBits;
+  const int64_t n = (int64_t)key.size();
+  uint64_t any = 0;
+  for (uint64_t k : key) any |= k;
+  int passes = 0;
+  while (passes < kMaxPasses && (any >> (passes * kBits)) != 0) ++passes;
+  std::vector<int64_t> count((size_t)passes * kDigits, 0);
+  for (uint64_t k : key)
+    for (int q = 0; q < passes; ++q) ++count[(size_t)q * kDigits + ((k >> (q * kBits)) & (kDigits - 1))];
+  std::vector<uint64_t> key2(n);
+  std::vector<int32_t> id2(id ? n : 0);
+  for (int q = 0; q < passes; ++q) {
+    int64_t *c = count.data() + (size_t)q * kDigits;
+    if (*std::max_element(c, c + kDigits) == n) continue;  // one digit value: order unchanged
+    int64_t sum = 0;
+    for (int d = 0; d < kDigits; ++d) {
+      const int64_t t = c[d];
+      c[d] = sum;
+      sum += t;
+    }
+    const int shift = q * kBits;
+    if (id) {
+      for (int64_t i = 0; i < n; ++i) {
+        const int64_t p = c[(key[i] >> shift) & (kDigits - 1)]++;
+        key2[p] = key[i];
+        id2[p] = (*id)[i];
+      }
+      id->swap(id2);
+    } else {
+      for (int64_t i = 0; i < n; ++i) key2[c[(key[i] >> shift) & (kDigits - 1)]++] = key[i];
+    }
+    key.swap(key2);
+  }
+}
+
+// Row boundaries of a sorted layout: offsets[k] = first position whose row
+// is >= k, for k = 0 .. rows.
+static std::vector<int32_t> offsets_of(const std::vector<int32_t> &row, int64_t rows) {
+  std::vector<int32_t> off(rows + 1);
+  int64_t p = 0;
+  const int64_t n = (int64_t)row.size();
+  for (int64_t k = 0; k <= rows; ++k) {
+    while (p < n && row[p] < k) ++p;
+    off[k] = (int32_t)p;
+  }
+  return off;
+}
+
 void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                    const int32_t *subj, const int32_t *rel, const int32_t *obj,
-                   const float *weight, bool keep_perm, bool keep_offsets, LayoutHost out[3]) {
+                   const float *weight, bool keep_perm, bool keep_offsets, LayoutHost out[3],
+                   LayoutSort how) {
+  // One 64-bit key per triple and order packs (row, second operand, first
+  // operand) as bit fields when 2 * bits(N_E - 1) + bits(N_R - 1) <= 64 (any
+  // KB up to 2^27 entities at 2^10 relations); otherwise three chained
+  // counting sorts per order.
+  auto bits = [](int64_t x) {
+    int b = 0;
+    while (b < 63 && (int64_t(1) << b) <= x) ++b;
+    return b;
+  };
+  const int be = bits(n_entities - 1), br = bits(n_relations - 1);
+  const bool radix = how == LayoutSort::kAuto && 2 * be + br <= 64;
+  if (radix && n_triples > 0) {
+    // Each order on its own thread (three at a time while their scratch,
+    // 16-24 bytes per triple each, stays modest).  The key holds the row,
+    // the second and the first operand: they are decoded from the sorted
+    // keys, and the triple ids are carried along only for the weights and
+    // the permutation.
+    const bool need_id = weight != nullptr || keep_perm;
+    auto one = [&](int which) {
+      const int64_t n = n_triples;
+      std::vector<uint64_t> key(n);
+      // key = major << (bits of middle + bits of minor) | middle << (bits of minor) | minor
+      const int32_t *major, *middle, *minor;
+      int b_mid;
+      int64_t rows;
+      if (which == BY_OBJ) {  // (o, r, s): row o, runs of r, A = s
+        major = obj, middle = rel, minor = subj, b_mid = br, rows = n_entities;
+      } else if (which == BY_SUBJ) {  // (s, r, o): row s, runs of r, A = o
+        major = subj, middle = rel, minor = obj, b_mid = br, rows = n_entities;
+      } else {  // (r, s, o): row r, runs of s, A = o
+        major = rel, middle = subj, minor = obj, b_mid = be, rows = n_relations;
+      }
+      const int s_mid = be, s_major = be + b_mid;
+      for (int64_t l = 0; l < n; ++l)
+        key[l] = ((uint64_t)major[l] << s_major) | ((uint64_t)middle[l] << s_mid) |
+                 (uint64_t)minor[l];
+      std::vector<int32_t> ids;
+      if (need_id) {
+        ids.resize(n);
+        for (int64_t l = 0; l < n; ++l) ids[l] = (int32_t)l;
+      }
+      radix_sort(key, need_id ? &ids : nullptr);
+      LayoutHost &L = out[which];
+      L.rows = rows;
+      L.row.resize(n);
+      L.col_a.resize(n);
+      L.col_b.resize(n);
+      const uint64_t m_minor = (uint64_t(1) << s_mid) - 1, m_mid = (uint64_t(1) << b_mid) - 1;
+      for (int64_t p = 0; p < n; ++p) {
+        const uint64_t k = key[p];
+        L.col_a[p] = (int32_t)(k & m_minor);
+        L.col_b[p] = (int32_t)((k >> s_mid) & m_mid);
+        L.row[p] = (int32_t)(k >> s_major);
+      }
+      std::vector<uint64_t>().swap(key);
+      if (weight) {
+        L.weight.resize(n);
+        for (int64_t p = 0; p < n; ++p) L.weight[p] = weight[ids[p]];
+      }
+      if (keep_offsets) L.offsets = offsets_of(L.row, rows);
+      if (keep_perm) L.perm = std::move(ids);
+    };
+    const bool parallel = n_triples <= (int64_t(1) << 27);
+    if (!parallel) {
+      for (int which : {BY_OBJ, BY_SUBJ, BY_REL}) one(which);
+      return;
+    }
+    std::exception_ptr err[3];
+    auto guarded = [&](int which) {
+      try {
+        one(which);
+      } catch (...) {
+        err[which] = std::current_exception();
+      }
+    };
+    std::thread t_subj(guarded, (int)BY_SUBJ), t_rel(guarded, (int)BY_REL);
+    guarded(BY_OBJ);
+    t_subj.join();
+    t_rel.join();
+    for (const auto &e : err)
+      if (e) std::rethrow_exception(e);
+    return;
+  }
   std::vector<int32_t> ident(n_triples), t1, t2, by_subj, by_obj, by_rel, count;
   for (int64_t l = 0; l < n_triples; ++l) ident[l] = (int32_t)l;
   std::vector<int32_t> off_subj, off_obj, off_rel;

@@ -88,12 +88,18 @@ std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_
                              const int32_t *subj, const int32_t *rel, const int32_t *obj,
                              bool *range_error);
 
+// How build_layouts sorts: kAuto takes the radix sort of a 64-bit key per
+// triple when N_E * N_R * N_E fits in 64 bits, else chained counting sorts;
+// kCounting forces the latter (both give the same stable orders).
+enum class LayoutSort { kAuto, kCounting };
+
 // Builds the three layouts.  keep_perm keeps the caller-index permutation,
 // keep_offsets the per-row boundaries (O(rows); the plans do not need them).
 // Everything else is O(N_T) plus, for dense id spaces, O(N_E + N_R).
 void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                    const int32_t *subj, const int32_t *rel, const int32_t *obj,
-                   const float *weight, bool keep_perm, bool keep_offsets, LayoutHost out[3]);
+                   const float *weight, bool keep_perm, bool keep_offsets, LayoutHost out[3],
+                   LayoutSort how = LayoutSort::kAuto);
 
 // Cuts a layout into chunks, marks the flush points and plans the combine levels.
 PlanHost plan_layout(const LayoutHost &layout, int32_t chunk, int32_t fan_in);

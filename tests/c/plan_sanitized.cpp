@@ -116,10 +116,17 @@ static void run_case(const char *what, int64_t n_e, int64_t n_r, std::vector<int
     w.resize(n_t);
     for (int64_t l = 0; l < n_t; ++l) w[l] = 0.5f + (float)(l % 7);
   }
-  LayoutHost L[3];
+  LayoutHost L[3], C[3];
   build_layouts(n_e, n_r, n_t, s.data(), r.data(), o.data(), weighted ? w.data() : nullptr, true,
                 true, L);
+  // The chained counting sorts give the same stable orders.
+  build_layouts(n_e, n_r, n_t, s.data(), r.data(), o.data(), weighted ? w.data() : nullptr, true,
+                true, C, LayoutSort::kCounting);
   for (int k = 0; k < 3; ++k) {
+    CHECK(L[k].rows == C[k].rows && L[k].row == C[k].row && L[k].col_a == C[k].col_a &&
+              L[k].col_b == C[k].col_b && L[k].weight == C[k].weight && L[k].perm == C[k].perm &&
+              L[k].offsets == C[k].offsets,
+          "%s: layout %d differs between the radix and the counting sorts", what, k);
     check_layout(L[k], n_t, what);
     for (int32_t chunk : {16, 24, 256}) {
       for (int32_t fan_in : {2, 3, 32}) check_plan(L[k], plan_layout(L[k], chunk, fan_in), chunk, what);
@@ -175,6 +182,20 @@ int main() {
       o[l] = l % 2 ? E(g) : (int32_t)(l % 7);
     }
     run_case("sparse ids", n_e, 4, s, r, o, true);
+  }
+  // Keys of exactly 64 bits (2 * 21 + 22 bits): the widest KB the radix sort
+  // takes, with the largest ids in every field; one relation more and the
+  // counting sorts take over.
+  for (int64_t n_r : {int64_t(1) << 22, (int64_t(1) << 22) + 1}) {
+    const int64_t n_e = int64_t(1) << 21, n_t = 5000;
+    std::uniform_int_distribution<int32_t> E(0, (int32_t)n_e - 1), R(0, (int32_t)n_r - 1);
+    std::vector<int32_t> s(n_t), r(n_t), o(n_t);
+    for (int64_t l = 0; l < n_t; ++l) {
+      s[l] = l % 4 ? E(g) : (int32_t)(n_e - 1);
+      r[l] = l % 5 ? R(g) : (int32_t)(n_r - 1);
+      o[l] = l % 6 ? E(g) : (int32_t)(n_e - 1 - l % 2);
+    }
+    run_case(n_r == (int64_t(1) << 22) ? "64-bit keys" : "65-bit keys", n_e, n_r, s, r, o, true);
   }
   // Empty KB; one entity with self-loops; one relation.
   run_case("empty", 7, 3, {}, {}, {}, false);
