@@ -7,7 +7,7 @@
 //   forward  Y  : rows = objects,   sum over r-runs of R[r] (.) sum X[s]   (Eq. 4)
 //   backward dX : rows = subjects,  sum over r-runs of R[r] (.) sum dY[o]
 //   backward dR : rows = relations, sum over s-runs of X[s] (.) sum dY[o]
-// so the planner sorts the triples three ways (counting sorts, stable) and
+// so the planner sorts the triples three ways (stable sorts) and
 // turns each sorted list into a stream of 8-byte entries cut into equal
 // chunks (see PlanHost).
 #pragma once
@@ -89,7 +89,8 @@ std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_
                              bool *range_error);
 
 // How build_layouts sorts: kAuto takes the radix sort of a 64-bit key per
-// triple when N_E * N_R * N_E fits in 64 bits, else chained counting sorts;
+// triple when 2 * bits(N_E - 1) + bits(N_R - 1) <= 64, else chained counting
+// sorts;
 // kCounting forces the latter (both give the same stable orders).
 enum class LayoutSort { kAuto, kCounting };
 
