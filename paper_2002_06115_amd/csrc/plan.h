@@ -90,8 +90,7 @@ std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_
 
 // How build_layouts sorts: kAuto takes the radix sort of a 64-bit key per
 // triple when 2 * bits(N_E - 1) + bits(N_R - 1) <= 64, else chained counting
-// sorts;
-// kCounting forces the latter (both give the same stable orders).
+// sorts; kCounting forces the latter (both give the same stable orders).
 enum class LayoutSort { kAuto, kCounting };
 
 // Builds the three layouts.  keep_perm keeps the caller-index permutation,
