@@ -6,9 +6,11 @@
 #include <climits>
 #include <cstdlib>
 #include <cstring>
+#include <exception>
 #include <initializer_list>
 #include <new>
 #include <string>
+#include <thread>
 #include <utility>
 #include <vector>
 
@@ -81,11 +83,13 @@ struct kb_t {
 
 namespace {
 
-template <class T>
-kb_status upload(kb_t *kb, const std::vector<T> &host, T **dev, hipStream_t s) {
+// Copies n elements of `host` into a new device allocation owned by the KB.
+template <class T, class D>
+kb_status upload(kb_t *kb, const T *host, size_t n, D **dev, hipStream_t s) {
+  static_assert(sizeof(T) == sizeof(D), "same element layout on both sides");
   *dev = nullptr;
-  if (host.empty()) return KB_OK;
-  const size_t bytes = host.size() * sizeof(T);
+  if (n == 0) return KB_OK;
+  const size_t bytes = n * sizeof(T);
   void *p = nullptr;
   hipError_t e = hipMalloc(&p, bytes);
   if (e != hipSuccess) {
@@ -94,10 +98,15 @@ kb_status upload(kb_t *kb, const std::vector<T> &host, T **dev, hipStream_t s) {
   }
   kb->allocations.push_back(p);
   kb->device_bytes += (int64_t)bytes;
-  e = hipMemcpyAsync(p, host.data(), bytes, hipMemcpyHostToDevice, s);
+  e = hipMemcpyAsync(p, host, bytes, hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
-  *dev = static_cast<T *>(p);
+  *dev = static_cast<D *>(p);
   return KB_OK;
+}
+
+template <class T, class D>
+kb_status upload(kb_t *kb, const std::vector<T> &host, D **dev, hipStream_t s) {
+  return upload(kb, host.data(), host.size(), dev, s);
 }
 
 void free_kb(kb_t *kb) {
@@ -110,10 +119,11 @@ void free_kb(kb_t *kb) {
   delete kb;
 }
 
-kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32_t chunk,
-                              int32_t fan_in, hipStream_t s) {
-  PlanHost P = plan_layout(H, chunk, fan_in);
-  D.rows = H.rows;
+// Uploads one layout's stream plan (made by plan_layout from its sorted
+// rows) and waits for the copies.
+kb_status build_device_layout(kb_t *kb, DevLayout &D, int64_t rows, const PlanHost &P,
+                              int32_t chunk, hipStream_t s) {
+  D.rows = rows;
   D.n = (int64_t)P.entries.size();
   D.chunk = chunk;
   D.n_chunks = P.n_chunks;
@@ -123,9 +133,7 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
   D.n_split_rows = P.n_split_rows;
   D.max_row_len = P.max_row_len;
   static_assert(sizeof(Entry) == sizeof(int2), "entry layout");
-  std::vector<int2> entries(D.n);
-  std::memcpy(entries.data(), P.entries.data(), D.n * sizeof(int2));
-  std::vector<Entry>().swap(P.entries);
+  static_assert(sizeof(EmptyPiece) == sizeof(int2), "empty-piece layout");
   std::vector<int4> ctasks;
   D.level_begin.assign(1, 0);
   for (const auto &lv : P.levels) {
@@ -133,15 +141,11 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, const LayoutHost &H, int32
     D.level_begin.push_back((int64_t)ctasks.size());
   }
   kb_status st;
-  if ((st = upload(kb, entries, &D.entries, s)) != KB_OK) return st;
+  if ((st = upload(kb, P.entries, &D.entries, s)) != KB_OK) return st;
   if ((st = upload(kb, P.weights, &D.weights, s)) != KB_OK) return st;
-  static_assert(sizeof(EmptyPiece) == sizeof(int2), "empty-piece layout");
-  std::vector<int2> pieces(P.empty.size());
-  if (!pieces.empty()) std::memcpy(pieces.data(), P.empty.data(), pieces.size() * sizeof(int2));
-  std::vector<EmptyPiece>().swap(P.empty);
-  if ((st = upload(kb, pieces, &D.empty, s)) != KB_OK) return st;
+  if ((st = upload(kb, P.empty, &D.empty, s)) != KB_OK) return st;
   if ((st = upload(kb, ctasks, &D.ctasks, s)) != KB_OK) return st;
-  // The host vectors die with this frame: wait for the copies first.
+  // The host vectors may die after this call: wait for the copies first.
   hipError_t e = hipStreamSynchronize(s);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   return KB_OK;
@@ -349,17 +353,33 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     {
       LayoutHost H[3];
       build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, weight, false, false, H);
+      // The three plans on three host threads, then the uploads in turn.
       const int32_t plen[3] = {chunk_seg, chunk_seg, chunk_rel};
+      PlanHost P[3];
+      std::exception_ptr err[3];
+      auto plan = [&](int k) {
+        try {
+          P[k] = plan_layout(H[k], plen[k], fan_in);
+          H[k] = LayoutHost{H[k].rows};  // the sorted rows are no longer needed
+        } catch (...) {
+          err[k] = std::current_exception();
+        }
+      };
+      {
+        std::thread t1(plan, 1), t2(plan, 2);
+        plan(0);
+        t1.join();
+        t2.join();
+      }
+      for (const auto &x : err)
+        if (x) std::rethrow_exception(x);
       for (int k = 0; k < 3; ++k) {
-        kb_status st = build_device_layout(kb, kb->L[k], H[k], plen[k], fan_in, s);
+        kb_status st = build_device_layout(kb, kb->L[k], H[k].rows, P[k], plen[k], s);
         if (st != KB_OK) {
           free_kb(kb);
           return st;
         }
-        std::vector<int32_t>().swap(H[k].row);
-        std::vector<int32_t>().swap(H[k].col_a);
-        std::vector<int32_t>().swap(H[k].col_b);
-        std::vector<float>().swap(H[k].weight);
+        P[k] = PlanHost{};
       }
     }
     *out = kb;
