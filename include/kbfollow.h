@@ -78,10 +78,23 @@ typedef enum {
  * The three sorted layouts (by object, by subject, by relation) and their
  * work plans are built on the host and uploaded; the host copies are freed.
  * Device memory held: 8 bytes per triple per layout (24 per triple; 36 with
- * weights) plus about 8 bytes per non-empty row per layout.  Building takes
- * seven stable counting passes over the triples.
+ * weights) plus about 8 bytes per non-empty row per layout.  Building sorts
+ * the triples three ways (radix sorts of one 64-bit key per triple when
+ * 2 * bits(N_E - 1) + bits(N_R - 1) <= 64, else chained counting sorts) on
+ * up to three host threads.
  * Errors: KB_EINVAL (sizes, null pointers), KB_ERANGE (an id out of range;
  * checked before any device work), KB_ENOMEM, KB_EHIP.
+ *
+ * Environment variables read here, for tests and tuning (results are the
+ * same up to the summation order of split rows, or bitwise the same):
+ *   KBFOLLOW_CHUNK, KBFOLLOW_REL_CHUNK  entries per chunk of the entity and
+ *                                       relation layouts (default 256, less
+ *                                       for small KBs; rounded up to 8);
+ *   KBFOLLOW_FAN_IN                     partials per combine task (32);
+ *   KBFOLLOW_PLAIN_LOADS=1              plain loads instead of raw buffer
+ *                                       loads (bitwise the same);
+ *   KBFOLLOW_LAYOUT_SORT=counting       the chained counting sorts for
+ *                                       every KB (bitwise the same).
  */
 kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                     const int32_t *subj, const int32_t *rel, const int32_t *obj,

@@ -352,7 +352,10 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
     {
       LayoutHost H[3];
-      build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, weight, false, false, H);
+      const char *how = std::getenv("KBFOLLOW_LAYOUT_SORT");
+      build_layouts(n_entities, n_relations, n_triples, subj, rel, obj, weight, false, false, H,
+                    how && std::strcmp(how, "counting") == 0 ? LayoutSort::kCounting
+                                                             : LayoutSort::kAuto);
       // The three plans on three host threads, then the uploads in turn.
       const int32_t plen[3] = {chunk_seg, chunk_seg, chunk_rel};
       PlanHost P[3];

@@ -101,12 +101,16 @@ def test_train_fullsize(kbf, integer):
 
 
 
-def test_maximum_entity_ids(kbf):
+@pytest.mark.parametrize("layout_sort", ["auto", "counting"])
+def test_maximum_entity_ids(kbf, layout_sort, monkeypatch):
     """N_E = 2^30, the largest id space the library takes, at b = 1 (4 GB per
     activation; tables of 4 GB or more take the plain-load path): triples at
     both ends of the id range, integer inputs, every row with a triple and a
-    sample of empty rows checked bit for bit against the oracle."""
+    sample of empty rows checked bit for bit against the oracle; layouts built
+    by the radix sorts (62-bit keys) and by the counting/comparison sorts."""
     import torch
+    if layout_sort == "counting":
+        monkeypatch.setenv("KBFOLLOW_LAYOUT_SORT", "counting")
     n_e, n_r, b = 1 << 30, 3, 1
     g = np.random.default_rng(30)
     n_t = 4000
