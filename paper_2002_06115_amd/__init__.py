@@ -84,6 +84,8 @@ def _load_library():
     lib.kb_layout_host.restype = ctypes.c_int
     lib.kb_profile_enable.argtypes = [p, i32]
     lib.kb_profile_enable.restype = ctypes.c_int
+    lib.kb_profile_select.argtypes = [p, ctypes.c_uint32]
+    lib.kb_profile_select.restype = ctypes.c_int
     lib.kb_profile_read.argtypes = [p, p, p]
     lib.kb_profile_read.restype = ctypes.c_int
     lib.kb_checked_violations.argtypes = [ctypes.POINTER(ctypes.c_uint64), i32]
@@ -272,8 +274,16 @@ class KB:
         return dX, dR
 
     # -- event timing -----------------------------------------------------------
-    def profile(self, on=True):
-        _check(_lib.kb_profile_enable(self._handle, 1 if on else 0), "kb_profile_enable")
+    def profile(self, on=True, phases=None):
+        """Record events around every phase's launches (on), none (off), or
+        only the phases named in `phases` (names from PHASES)."""
+        if phases is None:
+            _check(_lib.kb_profile_enable(self._handle, 1 if on else 0), "kb_profile_enable")
+            return
+        mask = 0
+        for p in phases:
+            mask |= 1 << PHASES.index(p)
+        _check(_lib.kb_profile_select(self._handle, mask if on else 0), "kb_profile_select")
 
     def profile_read(self):
         """{phase: (total ms, launches)} since the last read."""

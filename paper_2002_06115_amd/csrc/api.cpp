@@ -52,7 +52,7 @@ struct DevLayout {
 };
 
 struct Timing {
-  bool on = false;
+  uint32_t mask = 0;  // bit p set: phase p is recorded
   std::vector<hipEvent_t> pool;
   struct Rec {
     int phase;
@@ -168,7 +168,7 @@ struct PhaseScope {
     return e;
   }
   PhaseScope(const kb_t *k, int ph, hipStream_t st) : kb(k), phase(ph), s(st) {
-    if (!kb->timing.on) return;
+    if (!((kb->timing.mask >> phase) & 1u)) return;
     start = take(kb->timing);
     stop = take(kb->timing);
     if (start && stop) (void)hipEventRecord(start, s);
@@ -547,12 +547,16 @@ kb_status kb_checked_violations(uint64_t *count, int32_t reset) {
   return KB_OK;
 }
 
-kb_status kb_profile_enable(kb_t *kb, int32_t on) {
+kb_status kb_profile_select(kb_t *kb, uint32_t phase_mask) {
   if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
   kb_status st = kb_profile_read(kb, nullptr, nullptr);
   if (st != KB_OK) return st;
-  kb->timing.on = on != 0;
+  kb->timing.mask = phase_mask & ((1u << KB_PH_COUNT) - 1u);
   return KB_OK;
+}
+
+kb_status kb_profile_enable(kb_t *kb, int32_t on) {
+  return kb_profile_select(kb, on ? (1u << KB_PH_COUNT) - 1u : 0u);
 }
 
 kb_status kb_profile_read(kb_t *kb, double *ms, int64_t *launches) {
