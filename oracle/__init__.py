@@ -11,6 +11,8 @@ nothing from the product.
   double, for multi-hop chains.
 * :func:`follow_residual`, :func:`follow_backward_residual` -- the residual hop
   of the KB-completion chains (Sec. 3.2, App. E): follow(X, R) + gamma * X.
+* :func:`follow_accumulate` -- follow(X, R) + gamma * Z for any Z (the
+  residual hop with Z = X; adding into an existing output with Z = Y).
 * :mod:`oracle.chain` -- the three-hop chain with its softmax, L1 normalisation
   and cross-entropy loss, and the residual chain, forward and backward, in
   double.
@@ -55,9 +57,11 @@ def _load():
         lib.ora_follow_residual.argtypes = [i64, i64, i64, p, p, p, p, i32, p, p, f32, p, i32]
         lib.ora_follow_backward_residual.argtypes = [i64, i64, i64, p, p, p, p, i32, p, p, p, f32,
                                                      p, p, i32]
+        lib.ora_follow_accumulate.argtypes = [i64, i64, i64, p, p, p, p, i32, p, p, p, f32, p,
+                                              i32]
         for f in (lib.ora_follow, lib.ora_follow_backward, lib.ora_sampled, lib.ora_follow_f64,
                   lib.ora_follow_backward_f64, lib.ora_follow_residual,
-                  lib.ora_follow_backward_residual):
+                  lib.ora_follow_backward_residual, lib.ora_follow_accumulate):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -167,6 +171,22 @@ def follow_residual(subj, rel, obj, n_entities, n_relations, X, R, gamma=1.0, we
                                      _ptr(obj), _ptr(weight), b, _ptr(X), _ptr(R), gamma,
                                      _ptr(Y), nthreads)
     _check(rc, "follow_residual")
+    return Y
+
+
+def follow_accumulate(subj, rel, obj, n_entities, n_relations, X, R, Z, gamma=1.0, weight=None,
+                      nthreads=0):
+    """Y = follow(X, R) + gamma * Z (Z [b][N_E], any array of Y's shape),
+    rounded to float once."""
+    subj, rel, obj = _ids(subj), _ids(rel), _ids(obj)
+    X, R, Z, weight = _f32(X), _f32(R), _f32(Z), _f32(weight)
+    b = X.shape[0]
+    assert Z.shape == X.shape
+    Y = np.empty((b, n_entities), np.float32)
+    rc = _load().ora_follow_accumulate(n_entities, n_relations, len(subj), _ptr(subj), _ptr(rel),
+                                       _ptr(obj), _ptr(weight), b, _ptr(X), _ptr(R), _ptr(Z),
+                                       gamma, _ptr(Y), nthreads)
+    _check(rc, "follow_accumulate")
     return Y
 
 

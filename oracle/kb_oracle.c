@@ -298,6 +298,46 @@ int ora_follow_residual(int64_t n_e, int64_t n_r, int64_t n_t, const int32_t *su
   return err ? ORA_ENOMEM : ORA_OK;
 }
 
+/*
+ * Accumulating follow: Y[beta][j] = follow(X, R)[beta][j] + gamma * Z[beta][j]
+ * for any Z of Y's shape (Z = X is the residual hop above; Z = the old Y
+ * adds a hop's result into an existing output).  The per-triple sum first
+ * (caller order, double), then gamma * Z added in double, one rounding.  Y
+ * may be Z itself.  The gradient is follow's for X and R and gamma * dY for
+ * Z.
+ */
+int ora_follow_accumulate(int64_t n_e, int64_t n_r, int64_t n_t, const int32_t *subj,
+                          const int32_t *rel, const int32_t *obj, const float *w, int32_t b,
+                          const float *X, const float *R, const float *Z, float gamma, float *Y,
+                          int32_t nthreads) {
+  if (b < 0 || (b > 0 && (!X || !R || !Z || !Y))) return ORA_EINVAL;
+  int rc = check_ids(n_e, n_r, n_t, subj, rel, obj);
+  if (rc) return rc;
+  int err = 0;
+#pragma omp parallel num_threads(pick_threads(nthreads, b))
+  {
+    double *acc = (double *)malloc(sizeof(double) * (size_t)(n_e > 0 ? n_e : 1));
+    if (!acc) {
+#pragma omp atomic write
+      err = 1;
+    }
+#pragma omp for schedule(dynamic, 1)
+    for (int32_t beta = 0; beta < b; ++beta) {
+      if (!acc) continue;
+      const float *x = X + (size_t)beta * n_e;
+      const float *r = R + (size_t)beta * n_r;
+      const float *z = Z + (size_t)beta * n_e;
+      for (int64_t j = 0; j < n_e; ++j) acc[j] = 0.0;
+      for (int64_t l = 0; l < n_t; ++l)
+        acc[obj[l]] += weight_of(w, l) * (double)x[subj[l]] * (double)r[rel[l]];
+      float *y = Y + (size_t)beta * n_e;
+      for (int64_t j = 0; j < n_e; ++j) y[j] = (float)(acc[j] + (double)gamma * (double)z[j]);
+    }
+    free(acc);
+  }
+  return err ? ORA_ENOMEM : ORA_OK;
+}
+
 int ora_follow_backward_residual(int64_t n_e, int64_t n_r, int64_t n_t, const int32_t *subj,
                                  const int32_t *rel, const int32_t *obj, const float *w,
                                  int32_t b, const float *X, const float *R, const float *dY,

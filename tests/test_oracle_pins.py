@@ -417,6 +417,34 @@ def test_residual_hop_against_dense(gamma):
         assert np.array_equal(Y, oracle.follow(s, r, o, n_e, n_r, X, R, weight=w))
 
 
+@pytest.mark.parametrize("gamma", [0.0, 1.0, -0.75])
+def test_accumulate_against_dense(gamma):
+    """follow(X, R) + gamma * Z for an independent Z: the dense Eq. 4 plus
+    gamma * Z, rounded once; Z = X is the residual hop, gamma = 0 is follow."""
+    n_e, n_r, b = 36, 5, 6
+    s, r, o, w = tiny_kb(131, n_e, n_r, 280, weighted=True)
+    X, R, Z = rand_inputs(131, b, n_e, n_r, signed=True)
+    Y = oracle.follow_accumulate(s, r, o, n_e, n_r, X, R, Z, gamma, weight=w)
+    assert_rounded_once(Y, dense_ref.reified(s, r, o, n_e, n_r, X, R, w) + gamma * Z.astype(np.float64))
+    assert np.array_equal(oracle.follow_accumulate(s, r, o, n_e, n_r, X, R, X, gamma, weight=w),
+                          oracle.follow_residual(s, r, o, n_e, n_r, X, R, gamma, weight=w))
+    if gamma == 0.0:
+        assert np.array_equal(Y, oracle.follow(s, r, o, n_e, n_r, X, R, weight=w))
+
+
+def test_accumulate_integer_inputs_exact():
+    """On integer inputs every sum is exact: Y = counts + gamma * Z exactly."""
+    n_e, n_r, b = 40, 4, 5
+    s, r, o, _ = tiny_kb(7, n_e, n_r, 300)
+    g = np.random.default_rng(7)
+    X = g.integers(0, 3, (b, n_e)).astype(np.float32)
+    R = g.integers(0, 2, (b, n_r)).astype(np.float32)
+    Z = g.integers(-5, 6, (b, n_e)).astype(np.float32)
+    Y = oracle.follow_accumulate(s, r, o, n_e, n_r, X, R, Z, 2.0)
+    want = dense_ref.reified(s, r, o, n_e, n_r, X, R, None) + 2.0 * Z
+    assert np.array_equal(Y, want.astype(np.float32))
+
+
 def test_residual_chain_is_the_path_expansion():
     # App. E: with x^t = f^t(x^{t-1}) + x^{t-1}, x^T expands by linearity into
     # the sum, over every subset S of {1..T}, of the hops in S applied in order.
