@@ -167,6 +167,25 @@ kb_status kb_follow_backward_residual(const kb_t *kb, int32_t b, const float *X,
                                       const float *dY, float gamma, float *dX, float *dR,
                                       void *workspace, size_t ws_bytes, void *stream);
 
+/*
+ * Accumulating follow (the residual hop's added term from any array; the
+ * KB-completion hop of Sec. 3.2 / App. E is Z = X):
+ *   Y[j][beta] = follow(X, R)[j][beta] + gamma * Z[j][beta]
+ * summed in double and rounded to float once, like kb_follow.
+ *   Z : DEVICE [N_E][b] floats, aligned like X.  Z == Y adds the hop's
+ *       result into Y in place (each row of Z is read by the thread that
+ *       then writes that row of Y); otherwise Z must not overlap Y.  Z may
+ *       be X or overlap X or R (it is only read).
+ * Other arguments, the workspace and the errors as for kb_follow (KB_EINVAL
+ * also for a NULL Z or a Z that overlaps Y without being Y).  Raw buffer
+ * loads need the added rows to come from X, so with any other Z the
+ * forward pass takes the plain-load path (a few percent slower).  The
+ * gradient is kb_follow_backward's for X and R and gamma * dY for Z.
+ */
+kb_status kb_follow_accumulate(const kb_t *kb, int32_t b, const float *X, const float *R,
+                               const float *Z, float gamma, float *Y, void *workspace,
+                               size_t ws_bytes, void *stream);
+
 /* Static description of a status code. */
 const char *kb_status_str(kb_status s);
 

@@ -72,6 +72,8 @@ def _load_library():
     f32 = ctypes.c_float
     lib.kb_follow_residual.argtypes = [p, i32, p, p, f32, p, p, sz, p]
     lib.kb_follow_residual.restype = ctypes.c_int
+    lib.kb_follow_accumulate.argtypes = [p, i32, p, p, p, f32, p, p, sz, p]
+    lib.kb_follow_accumulate.restype = ctypes.c_int
     lib.kb_follow_backward_residual.argtypes = [p, i32, p, p, p, f32, p, p, p, sz, p]
     lib.kb_follow_backward_residual.restype = ctypes.c_int
     lib.kb_status_str.argtypes = [ctypes.c_int]
@@ -237,6 +239,27 @@ class KB:
                                                float(residual), self._ptr(Y), self._ptr(ws), nws,
                                                ctypes.c_void_p(s.cuda_stream)),
                        "kb_follow_residual")
+        return Y
+
+    def follow_accumulate(self, X, R, Z, gamma=1.0, out=None, stream=None):
+        """Y = follow(X, R) + gamma * Z for Z [N_E][b]; ``out=Z`` adds the hop
+        into Z in place.  The gradient with respect to Z is gamma * dY."""
+        import torch
+        X = self._act(X, self.n_entities, "X")
+        R = self._act(R, self.n_relations, "R")
+        Z = self._act(Z, self.n_entities, "Z")
+        b = X.shape[1]
+        if R.shape[1] != b or Z.shape[1] != b:
+            raise ValueError("X, R and Z must have the same batch size")
+        Y = torch.empty_like(X) if out is None else self._act(out, self.n_entities, "out")
+        s = torch.cuda.current_stream(self.device) if stream is None else stream
+        ws = self.workspace(b, s)
+        nws = 0 if ws is None else ws.numel()
+        with torch.cuda.device(self.device):
+            _check(_lib.kb_follow_accumulate(self._handle, b, self._ptr(X), self._ptr(R),
+                                             self._ptr(Z), float(gamma), self._ptr(Y),
+                                             self._ptr(ws), nws, ctypes.c_void_p(s.cuda_stream)),
+                   "kb_follow_accumulate")
         return Y
 
     def follow_backward(self, X, R, dY, want_dx=True, want_dr=True, dX=None, dR=None,

@@ -204,18 +204,18 @@ kb_status check_device(const kb_t *kb) {
 }
 
 // Runs one pass: the stream kernel, the first combine level together with
-// the empty rows, the further combine levels.  With
-// residual set (A has one row per output row) every output row j also gets
-// gamma * A[j].
+// the empty rows, the further combine levels.  With Z non-null (one row per
+// output row; A itself for the residual hop, out itself to add in place)
+// every output row j also gets gamma * Z[j].
 kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float *A,
                    int64_t A_rows, const float *B, int64_t B_rows, int32_t b, float *out,
-                   void *ws, bool residual, float gamma, hipStream_t s) {
+                   void *ws, const float *Z, float gamma, hipStream_t s) {
   double *slots = static_cast<double *>(ws);
-  const float *res = residual ? A : nullptr;
+  const float *res = Z;
   {
     PhaseScope scope(kb, ph_base + 0, s);
-    StreamArgs a{D.entries, D.weights, D.n, D.chunk, A, A_rows, B, B_rows, b, out, D.rows,
-                 slots, D.n_slots, residual ? 1 : 0, gamma};
+    StreamArgs a{D.entries, D.weights, D.n, D.chunk, A,           A_rows,     B,
+                 B_rows,    b,         out,  D.rows,  slots, D.n_slots, Z ? 1 : 0, gamma, Z};
     hipError_t e = launch_stream(a, kb->plain_loads, s);
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
@@ -430,7 +430,8 @@ kb_status kb_get_info(const kb_t *kb, kb_info_t *info) {
 
 namespace {
 
-kb_status follow_impl(const kb_t *kb, int32_t b, const float *X, const float *R, bool residual,
+// Y = follow(X, R) [+ gamma * Z when Z is non-null].
+kb_status follow_impl(const kb_t *kb, int32_t b, const float *X, const float *R, const float *Z,
                       float gamma, float *Y, void *workspace, size_t ws_bytes, void *stream) {
   try {
     if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
@@ -440,19 +441,24 @@ kb_status follow_impl(const kb_t *kb, int32_t b, const float *X, const float *R,
     if ((ent_bytes && (!X || !Y)) || (rel_bytes && !R))
       return fail(KB_EINVAL, "X, R and Y must be non-NULL");
     const size_t al = (b % 4 == 0) ? 16 : 4;
-    if ((X && !aligned(X, al)) || (R && !aligned(R, al)) || (Y && !aligned(Y, al)))
-      return fail(KB_EINVAL, "X, R and Y must be " + std::to_string(al) + "-byte aligned");
+    if ((X && !aligned(X, al)) || (R && !aligned(R, al)) || (Y && !aligned(Y, al)) ||
+        (Z && !aligned(Z, al)))
+      return fail(KB_EINVAL, "X, R, Z and Y must be " + std::to_string(al) + "-byte aligned");
     if (overlaps(Y, ent_bytes, X, ent_bytes) || overlaps(Y, ent_bytes, R, rel_bytes))
       return fail(KB_EINVAL, "Y overlaps X or R");
-    kb_status st =
-        check_ws(kb, b, workspace, ws_bytes, {{X, ent_bytes}, {R, rel_bytes}, {Y, ent_bytes}});
+    // Row j of Z is read by the thread that then writes row j of Y: Z may be
+    // Y itself, but not overlap it otherwise.
+    if (Z != Y && overlaps(Z, ent_bytes, Y, ent_bytes))
+      return fail(KB_EINVAL, "Z overlaps Y without being Y");
+    kb_status st = check_ws(kb, b, workspace, ws_bytes,
+                            {{X, ent_bytes}, {R, rel_bytes}, {Y, ent_bytes}, {Z, ent_bytes}});
     if (st != KB_OK) return st;
     if ((st = check_device(kb)) != KB_OK) return st;
     g_last_error.clear();
     if (!ent_bytes) return KB_OK;
     // By object, runs of equal relation: Y[o] = sum over runs of R[r] (.) sum of X[s].
     return run_pass(kb, kb->L[BY_OBJ], KB_PH_FWD_STREAM, X, kb->n_entities, R, kb->n_relations,
-                    b, Y, workspace, residual, gamma, static_cast<hipStream_t>(stream));
+                    b, Y, workspace, Z, gamma, static_cast<hipStream_t>(stream));
   } catch (...) {
     return fail(KB_EINVAL, "unexpected host error");
   }
@@ -493,13 +499,13 @@ kb_status backward_impl(const kb_t *kb, int32_t b, const float *X, const float *
       // By subject, runs of equal relation: dX[s] = sum over runs of R[r] (.) sum of dY[o]
       // (+ gamma * dY[s] for the residual hop).
       st = run_pass(kb, kb->L[BY_SUBJ], KB_PH_DX_STREAM, dY, kb->n_entities, R, kb->n_relations,
-                    b, dX, workspace, residual, gamma, s);
+                    b, dX, workspace, residual ? dY : nullptr, gamma, s);
       if (st != KB_OK) return st;
     }
     if (want_dr) {
       // By relation, runs of equal subject: dR[k] = sum over runs of X[s] (.) sum of dY[o].
       st = run_pass(kb, kb->L[BY_REL], KB_PH_DR_STREAM, dY, kb->n_entities, X, kb->n_entities,
-                    b, dR, workspace, false, 0.0f, s);
+                    b, dR, workspace, nullptr, 0.0f, s);
       if (st != KB_OK) return st;
     }
     return KB_OK;
@@ -514,13 +520,20 @@ extern "C" {
 
 kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, float *Y,
                     void *workspace, size_t ws_bytes, void *stream) {
-  return follow_impl(kb, b, X, R, false, 0.0f, Y, workspace, ws_bytes, stream);
+  return follow_impl(kb, b, X, R, nullptr, 0.0f, Y, workspace, ws_bytes, stream);
 }
 
 kb_status kb_follow_residual(const kb_t *kb, int32_t b, const float *X, const float *R,
                              float gamma, float *Y, void *workspace, size_t ws_bytes,
                              void *stream) {
-  return follow_impl(kb, b, X, R, true, gamma, Y, workspace, ws_bytes, stream);
+  return follow_impl(kb, b, X, R, X, gamma, Y, workspace, ws_bytes, stream);
+}
+
+kb_status kb_follow_accumulate(const kb_t *kb, int32_t b, const float *X, const float *R,
+                               const float *Z, float gamma, float *Y, void *workspace,
+                               size_t ws_bytes, void *stream) {
+  if (kb && kb->n_entities > 0 && !Z) return fail(KB_EINVAL, "Z must be non-NULL");
+  return follow_impl(kb, b, X, R, Z, gamma, Y, workspace, ws_bytes, stream);
 }
 
 kb_status kb_follow_backward_residual(const kb_t *kb, int32_t b, const float *X, const float *R,

@@ -28,9 +28,12 @@ constexpr int32_t kChunkQuantum = 8;
 //     acc += w[p] * A[a] (.) held             for every triple
 //     target = acc (float row / double slot), acc = 0   at a marker
 // A has A_rows rows and B has B_rows rows of b floats.  With `residual` set
-// (A then has one row per output row), a marker writing row j writes
-// acc + gamma * A[j] instead: the residual hop follow(X, R) + gamma * X of the
-// KB-completion chains, and its dX pass (A = dY there).
+// a marker writing row j writes acc + gamma * Z[j] instead (Z has out_rows
+// rows): with Z = A the residual hop follow(X, R) + gamma * X of the
+// KB-completion chains and its dX pass (A = dY there); with any other Z the
+// accumulating follow, Z = out itself adding into the output in place (each
+// row's Z is read by the thread that then writes it).  Raw buffer loads need
+// Z = A; another Z takes the plain-load path.
 struct StreamArgs {
   const int2 *entries;
   const float *weights;  // per entry, nullptr for a hard KB
@@ -47,13 +50,15 @@ struct StreamArgs {
   int64_t n_slots;
   int32_t residual;
   float gamma;
+  const float *Z;  // the rows added at markers when residual is set
 };
 // plain_loads forces the plain-load variant (used anyway for tables of 4 GB
 // or more) so it can be tested at small sizes.
 hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s);
 
 // Sums workspace slots in order (one combine level).  A final row write adds
-// gamma * res[row] when res is not null (residual hop).
+// gamma * res[row] when res is not null (residual hop, accumulating follow;
+// res may be out itself).
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int64_t n_slots,
                           int32_t b, float *out, int64_t out_rows, const float *res, float gamma,
                           hipStream_t s);

@@ -292,7 +292,12 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
                                          : kOutOfRange,
                                xb[u]);
         } else {
-          load_row<VEC>(a.A + (size_t)(triple || res_row ? KBF_CHECKED(ia, a.A_rows) : 0) * bb + cl,
+          // A residual row comes from Z (A itself for the residual hop).
+          const float *src = res_row ? a.Z : a.A;
+          load_row<VEC>(src + (size_t)(triple ? KBF_CHECKED(ia, a.A_rows)
+                                              : res_row ? KBF_CHECKED(ia, a.out_rows) : 0) *
+                                  bb +
+                              cl,
                         xa[u]);
           load_row<VEC>(a.B + (size_t)(run_start ? KBF_CHECKED(e[u].y, a.B_rows) : 0) * bb + cl,
                         xb[u]);
@@ -351,9 +356,9 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
 template <int VEC, int LPT>
 __device__ __forceinline__ void combine_tasks(const int4 *__restrict__ tasks, int64_t n_tasks,
                                               double *__restrict__ slots, int64_t n_slots,
-                                              int32_t b, float *__restrict__ out,
-                                              int64_t out_rows, const float *__restrict__ res,
-                                              float gamma, int64_t block, int64_t n_blocks) {
+                                              int32_t b, float *out, int64_t out_rows,
+                                              const float *res, float gamma, int64_t block,
+                                              int64_t n_blocks) {
   constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
   const int lane = threadIdx.x % LPT;
@@ -405,9 +410,9 @@ __device__ __forceinline__ void combine_tasks(const int4 *__restrict__ tasks, in
 // `block` of `n_blocks` blocks share the pieces.
 template <int VEC, int LPT, bool PACKED>
 __device__ __forceinline__ void zero_pieces(const int2 *__restrict__ pieces, int64_t n_pieces,
-                                            int32_t b, float *__restrict__ out, int64_t out_rows,
-                                            const float *__restrict__ res, float gamma,
-                                            int64_t block, int64_t n_blocks) {
+                                            int32_t b, float *out, int64_t out_rows,
+                                            const float *res, float gamma, int64_t block,
+                                            int64_t n_blocks) {
   constexpr int W = LPT * VEC;
   constexpr int GPB = kBlock / LPT;
   const int lane = threadIdx.x % LPT;
@@ -458,9 +463,8 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const int4 *__restrict_
                                                          int64_t n_tasks,
                                                          double *__restrict__ slots,
                                                          int64_t n_slots, int32_t b,
-                                                         float *__restrict__ out, int64_t out_rows,
-                                                         const float *__restrict__ res,
-                                                         float gamma) {
+                                                         float *out, int64_t out_rows,
+                                                         const float *res, float gamma) {
   combine_tasks<VEC, LPT>(tasks, n_tasks, slots, n_slots, b, out, out_rows, res, gamma,
                           blockIdx.x, gridDim.x);
 }
@@ -561,7 +565,8 @@ hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
   // Raw-buffer offsets are 32-bit: tables of 4 GB or more take plain loads.
   const uint64_t row_bytes = (uint64_t)a.b * sizeof(float);
   const uint64_t lim = kOutOfRange;
-  const bool buf = !plain_loads && (uint64_t)a.A_rows * row_bytes <= lim &&
+  const bool buf = !plain_loads && (!a.residual || a.Z == a.A) &&
+                   (uint64_t)a.A_rows * row_bytes <= lim &&
                    (uint64_t)a.B_rows * row_bytes <= lim && (uint64_t)a.out_rows * row_bytes <= lim &&
                    (uint64_t)a.n_slots * (uint64_t)a.b * sizeof(double) <= lim;
   const void *fn = stream_fn_for(t, buf, a.weights != nullptr, a.residual != 0);
