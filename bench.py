@@ -74,18 +74,37 @@ def pass_bytes(kb, b, phase, whole_pass=False):
     return float(gather), float(comp), float(once)
 
 
-def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False):
-    """Mangled name of the stream-kernel instance a pass launches for batch b:
-    VEC = 4 floats per lane when b % 4 == 0 (else 1), LPT = lanes per group
-    (b / VEC rounded up to a power of two, at most 64), raw-buffer loads unless
-    a table reaches 4 GB."""
+def column_tiling(b):
+    """(VEC, LPT): 4 floats per lane when b % 4 == 0 (else 1), lanes per group
+    b / VEC rounded up to a power of two, at most 64."""
     vec = 4 if b % 4 == 0 else 1
     lanes, lpt = -(-b // vec), 1
     while lpt < lanes and lpt < 64:
         lpt *= 2
+    return vec, lpt
+
+
+MAX_LDS_B = 80 * 1024  # largest B column slice the stream kernel stages in LDS
+
+
+def b_slice_fits_lds(b, b_rows):
+    """Whether a pass's B table (b_rows rows; R for forward and dX, X for dR)
+    is small enough for the LDS variant.  The library also needs two of its
+    workgroups to fit a CU, which holds for the hard-KB, non-residual
+    variants at b >= 32."""
+    vec, lpt = column_tiling(b)
+    return b_rows * vec * lpt * 4 <= MAX_LDS_B
+
+
+def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False, lds=False):
+    """Mangled name of the stream-kernel instance a pass launches for batch b:
+    lane layout from column_tiling, raw-buffer loads unless a table reaches
+    4 GB, B staged in LDS (lds) or held in registers."""
+    vec, lpt = column_tiling(b)
     flag = lambda v: 1 if v else 0
     return (f"_ZN3kbf12_GLOBAL__N_113stream_kernelILi{vec}ELi{lpt}ELb{flag(not plain_loads)}"
-            f"ELb{flag(weighted)}ELb{flag(residual)}EEEvNS_10StreamArgsE")
+            f"ELb{flag(weighted)}ELb{flag(residual)}ELb{flag(lds and not plain_loads)}"
+            f"EEEvNS_10StreamArgsE")
 
 
 def measured_traffic(workload, b, phase, symbol):
@@ -494,8 +513,11 @@ def main():
         ms_avg = dom_timed[0] / max(1, dom_timed[1])
         gather_b, comp_b, once_b = pass_bytes(kb, b, dom)
         sec = ms_avg * 1e-3
+        b_rows = w.n_entities if dom == "dr_stream" else w.n_relations
         symbol = stream_kernel_symbol(b, residual=args.residual is not None,
-                                      plain_loads=os.environ.get("KBFOLLOW_PLAIN_LOADS") == "1")
+                                      plain_loads=os.environ.get("KBFOLLOW_PLAIN_LOADS") == "1",
+                                      lds=os.environ.get("KBFOLLOW_B_IN_LDS") != "0"
+                                      and b_slice_fits_lds(b, b_rows))
         traffic = measured_traffic(w.name, b, dom, symbol)
         roof = {"bound": "hbm", "achieved": round(comp_b / sec / 1e9, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(comp_b / sec / 1e9 / PEAK_HBM_GBPS, 4),

@@ -75,6 +75,7 @@ struct kb_t {
   int64_t n_entities = 0, n_relations = 0, n_triples = 0;
   bool weighted = false;
   bool plain_loads = false;  // force plain loads instead of raw buffer loads (testing)
+  bool b_in_lds = true;      // stage small B tables in LDS (off: B rows in registers)
   DevLayout L[3];
   std::vector<void *> allocations;
   int64_t device_bytes = 0;
@@ -216,7 +217,11 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
     PhaseScope scope(kb, ph_base + 0, s);
     StreamArgs a{D.entries, D.weights, D.n, D.chunk, A,           A_rows,     B,
                  B_rows,    b,         out,  D.rows,  slots, D.n_slots, Z ? 1 : 0, gamma, Z};
-    hipError_t e = launch_stream(a, kb->plain_loads, s);
+    StreamOptions o;
+    o.plain_loads = kb->plain_loads;
+    o.b_in_lds = kb->b_in_lds;
+    o.n_cu = kb->n_cu;
+    hipError_t e = launch_stream(a, o, s);
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
   {
@@ -330,6 +335,7 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
       kb->n_cu = v;
     if (kb->n_cu <= 0) kb->n_cu = 1;
     kb->plain_loads = env_int("KBFOLLOW_PLAIN_LOADS", 0) != 0;
+    kb->b_in_lds = env_int("KBFOLLOW_B_IN_LDS", 1) != 0;
     kb->n_entities = n_entities;
     kb->n_relations = n_relations;
     kb->n_triples = n_triples;

@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstddef>
 #include <cstdint>
 
 namespace kbf {
@@ -52,9 +53,20 @@ struct StreamArgs {
   float gamma;
   const float *Z;  // the rows added at markers when residual is set
 };
-// plain_loads forces the plain-load variant (used anyway for tables of 4 GB
-// or more) so it can be tested at small sizes.
-hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s);
+// Largest B column slice (B_rows * slice width * 4 bytes) the stream kernel
+// copies into LDS: two copies fit a CU's 160 KB.
+constexpr size_t kMaxLdsB = 80 * 1024;
+
+struct StreamOptions {
+  // Forces the plain-load variant (used anyway for tables of 4 GB or more)
+  // so it can be tested at small sizes.
+  bool plain_loads = false;
+  // Stage B in LDS when its slice fits kMaxLdsB (raw-buffer path only);
+  // off keeps B rows in registers, the variant used for larger tables.
+  bool b_in_lds = true;
+  int n_cu = 1;  // compute units of the device, for the LDS variant's grid
+};
+hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s);
 
 // Sums workspace slots in order (one combine level).  A final row write adds
 // gamma * res[row] when res is not null (residual hop, accumulating follow;

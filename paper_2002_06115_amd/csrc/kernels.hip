@@ -32,6 +32,8 @@
 #include "plan.h"
 
 #include <climits>
+#include <map>
+#include <mutex>
 #include <utility>
 
 namespace kbf {
@@ -39,6 +41,10 @@ namespace kbf {
 namespace {
 
 constexpr int kBlock = 256;   // threads per workgroup (4 wavefronts of 64)
+// Workgroup of the stream kernel when the B table sits in LDS: 12 waves, so
+// that two workgroups (two copies of the table, up to kMaxLdsB bytes each)
+// fill a CU at the six waves per SIMD that the kernel's registers allow.
+constexpr int kBlockLds = 768;
 constexpr int kUnroll = 8;    // entries per step; a lane group keeps their loads in flight
 static_assert(kChunkQuantum % kUnroll == 0, "a chunk is a whole number of steps");
 
@@ -118,6 +124,27 @@ __device__ __forceinline__ void load_row_buffer(__amdgpu_buffer_rsrc_t rsrc, uin
 }
 
 typedef float native_float4 __attribute__((ext_vector_type(4)));
+
+// VEC floats of LDS at p (16-byte aligned when VEC = 4).
+template <int VEC>
+__device__ __forceinline__ void lds_row(const float *p, float (&v)[VEC]) {
+  if constexpr (VEC == 4) {
+    const native_float4 t = *reinterpret_cast<const native_float4 *>(p);
+    v[0] = t[0];
+    v[1] = t[1];
+    v[2] = t[2];
+    v[3] = t[3];
+  } else {
+    v[0] = *p;
+  }
+}
+template <int VEC>
+__device__ __forceinline__ void lds_store(float *p, const float (&v)[VEC]) {
+  if constexpr (VEC == 4)
+    *reinterpret_cast<native_float4 *>(p) = native_float4{v[0], v[1], v[2], v[3]};
+  else
+    *p = v[0];
+}
 
 // Output rows are written once and not read again by the pass: non-temporal
 // stores keep them from displacing gathered rows in the caches.
@@ -204,9 +231,20 @@ __device__ __forceinline__ void store_row_buffer(__amdgpu_buffer_rsrc_t rsrc, ui
 // marker therefore finds A = 0 and a held B row of 0, so its FMA adds an
 // exact zero.  Without BUF, plain loads read row 0 at markers and the values
 // are masked instead.
-template <int VEC, int LPT, bool BUF, bool WEIGHTED, bool RES>
-__global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
-  constexpr int GPB = kBlock / LPT;
+//
+// With LDSB (raw buffer loads only) the workgroup first copies its column
+// slice of the whole B table into LDS, and a run start reads its B row from
+// there when the FMAs need it.  No B row is then held in registers while a
+// step's gathers are in flight, which leaves room for more waves per SIMD,
+// and the B reads leave the L2 alone.  Used when the table fits (R for the
+// forward and dX passes, at most kMaxLdsB bytes per slice).
+template <int VEC, int LPT, bool BUF, bool WEIGHTED, bool RES, bool LDSB>
+__global__ __launch_bounds__(LDSB ? kBlockLds : kBlock) void stream_kernel(StreamArgs a) {
+  static_assert(BUF || !LDSB, "the LDS copy of B goes with raw buffer loads");
+  constexpr int BLK = LDSB ? kBlockLds : kBlock;
+  constexpr int GPB = BLK / LPT;
+  constexpr int W = LPT * VEC;  // columns of one slice
+  extern __shared__ float b_lds[];  // [B_rows][W] with LDSB
   const int lane = threadIdx.x % LPT;
   const int grp = threadIdx.x / LPT;
   const int c = blockIdx.y * (LPT * VEC) + lane * VEC;
@@ -230,6 +268,25 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
 
   const int64_t n_chunks = a.n / a.chunk;
   const int64_t stride = (int64_t)gridDim.x * GPB;
+
+  if constexpr (LDSB) {
+    // Columns [col0, col0 + W) of every B row; columns past b read as zeros.
+    const int col0 = blockIdx.y * W;
+    const int64_t n_lds = a.B_rows * W;
+    for (int64_t i = (int64_t)threadIdx.x * VEC; i < n_lds; i += (int64_t)BLK * VEC) {
+      const int64_t r = i / W;
+      const int j = (int)(i % W);
+      float v[VEC];
+      if (col0 + j < a.b) {
+        load_row<VEC>(a.B + (size_t)KBF_CHECKED(r, a.B_rows) * bb + col0 + j, v);
+      } else {
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) v[q] = 0.0f;
+      }
+      lds_store<VEC>(b_lds + i, v);
+    }
+    __syncthreads();
+  }
 
   // Each lane loads K of a step's kUnroll entries (lane + k * LPT) and the
   // group shares them by broadcast, so one load instruction fetches the
@@ -286,11 +343,12 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
                                    ? (uint32_t)KBF_CHECKED(ia, a.A_rows) * row_bytes + col_bytes
                                    : kOutOfRange,
                                xa[u]);
-          load_row_buffer<VEC>(brsrc,
-                               run_start ? (uint32_t)KBF_CHECKED(e[u].y, a.B_rows) * row_bytes +
-                                               col_bytes
-                                         : kOutOfRange,
-                               xb[u]);
+          if constexpr (!LDSB)
+            load_row_buffer<VEC>(brsrc,
+                                 run_start ? (uint32_t)KBF_CHECKED(e[u].y, a.B_rows) * row_bytes +
+                                                 col_bytes
+                                           : kOutOfRange,
+                                 xb[u]);
         } else {
           // A residual row comes from Z (A itself for the residual hop).
           const float *src = res_row ? a.Z : a.A;
@@ -310,11 +368,20 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(StreamArgs a) {
         const bool run_start = triple && (e[u].x & kRunStart);
         // Run starts take the new B row; markers take the zeros their
         // out-of-range B load returned (masked explicitly without BUF).
-        const bool take_b = run_start || !triple;
+        if constexpr (LDSB) {
+          if (run_start) {
+            lds_row<VEC>(b_lds + (size_t)KBF_CHECKED(e[u].y, a.B_rows) * W + lane * VEC, held_b);
+          } else if (!triple) {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) held_b[v] = 0.0f;
+          }
+        }
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
-          const float nb = (BUF || triple) ? xb[u][v] : 0.0f;
-          held_b[v] = take_b ? nb : held_b[v];
+          if constexpr (!LDSB) {
+            const float nb = (BUF || triple) ? xb[u][v] : 0.0f;
+            held_b[v] = (run_start || !triple) ? nb : held_b[v];
+          }
           double t = (double)xa[u][v];
           if constexpr (WEIGHTED) t *= (double)w[u];
           // Zero at markers (also the residual row's A and plain loads' row 0).
@@ -484,30 +551,60 @@ __global__ __launch_bounds__(kBlock) void tail_kernel(TailArgs a) {
                                   (int64_t)gridDim.x - a.combine_blocks);
 }
 
-template <int VEC, bool BUF, bool WT, bool RES>
+template <int VEC, bool BUF, bool WT, bool RES, bool LDSB>
 const void *stream_fn(int lpt) {
   switch (lpt) {
-    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, BUF, WT, RES>);
-    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, BUF, WT, RES>);
-    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, BUF, WT, RES>);
-    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, BUF, WT, RES>);
-    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, BUF, WT, RES>);
-    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, BUF, WT, RES>);
-    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, BUF, WT, RES>);
+    case 1: return reinterpret_cast<const void *>(&stream_kernel<VEC, 1, BUF, WT, RES, LDSB>);
+    case 2: return reinterpret_cast<const void *>(&stream_kernel<VEC, 2, BUF, WT, RES, LDSB>);
+    case 4: return reinterpret_cast<const void *>(&stream_kernel<VEC, 4, BUF, WT, RES, LDSB>);
+    case 8: return reinterpret_cast<const void *>(&stream_kernel<VEC, 8, BUF, WT, RES, LDSB>);
+    case 16: return reinterpret_cast<const void *>(&stream_kernel<VEC, 16, BUF, WT, RES, LDSB>);
+    case 32: return reinterpret_cast<const void *>(&stream_kernel<VEC, 32, BUF, WT, RES, LDSB>);
+    case 64: return reinterpret_cast<const void *>(&stream_kernel<VEC, 64, BUF, WT, RES, LDSB>);
   }
   return nullptr;
 }
 
-template <int VEC, bool BUF>
-const void *stream_fn_buf(int lpt, bool wt, bool res) {
-  if (wt) return res ? stream_fn<VEC, BUF, true, true>(lpt) : stream_fn<VEC, BUF, true, false>(lpt);
-  return res ? stream_fn<VEC, BUF, false, true>(lpt) : stream_fn<VEC, BUF, false, false>(lpt);
+template <int VEC, bool BUF, bool LDSB>
+const void *stream_fn_sel(int lpt, bool wt, bool res) {
+  if (wt)
+    return res ? stream_fn<VEC, BUF, true, true, LDSB>(lpt)
+               : stream_fn<VEC, BUF, true, false, LDSB>(lpt);
+  return res ? stream_fn<VEC, BUF, false, true, LDSB>(lpt)
+             : stream_fn<VEC, BUF, false, false, LDSB>(lpt);
 }
 
-const void *stream_fn_for(const ColumnTiling &t, bool buf, bool wt, bool res) {
-  if (t.vec == 4)
-    return buf ? stream_fn_buf<4, true>(t.lpt, wt, res) : stream_fn_buf<4, false>(t.lpt, wt, res);
-  return buf ? stream_fn_buf<1, true>(t.lpt, wt, res) : stream_fn_buf<1, false>(t.lpt, wt, res);
+// Plain loads never take the LDS copy of B.
+const void *stream_fn_for(const ColumnTiling &t, bool buf, bool lds, bool wt, bool res) {
+  if (t.vec == 4) {
+    if (!buf) return stream_fn_sel<4, false, false>(t.lpt, wt, res);
+    return lds ? stream_fn_sel<4, true, true>(t.lpt, wt, res)
+               : stream_fn_sel<4, true, false>(t.lpt, wt, res);
+  }
+  if (!buf) return stream_fn_sel<1, false, false>(t.lpt, wt, res);
+  return lds ? stream_fn_sel<1, true, true>(t.lpt, wt, res)
+             : stream_fn_sel<1, true, false>(t.lpt, wt, res);
+}
+
+// Workgroups of `fn` (kBlockLds threads, lds_bytes of dynamic LDS) that fit
+// one CU at once, from the runtime's occupancy calculator; cached per kernel
+// and LDS size.  0 when the query fails.
+int lds_blocks_per_cu(const void *fn, size_t lds_bytes) {
+  static std::mutex mu;
+  static std::map<std::pair<const void *, size_t>, int> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_pair(fn, lds_bytes);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int n = 0;
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsB) !=
+          hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kBlockLds, lds_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    n = 0;
+  }
+  cache[key] = n;
+  return n;
 }
 
 template <int VEC>
@@ -559,23 +656,43 @@ ColumnTiling column_tiling(int32_t b) {
   return t;
 }
 
-hipError_t launch_stream(const StreamArgs &a, bool plain_loads, hipStream_t s) {
+hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   const ColumnTiling t = column_tiling(a.b);
+  if (a.chunk % kChunkQuantum != 0 || a.n % a.chunk != 0) return hipErrorInvalidValue;
   // Raw-buffer offsets are 32-bit: tables of 4 GB or more take plain loads.
   const uint64_t row_bytes = (uint64_t)a.b * sizeof(float);
   const uint64_t lim = kOutOfRange;
-  const bool buf = !plain_loads && (!a.residual || a.Z == a.A) &&
+  const bool buf = !o.plain_loads && (!a.residual || a.Z == a.A) &&
                    (uint64_t)a.A_rows * row_bytes <= lim &&
                    (uint64_t)a.B_rows * row_bytes <= lim && (uint64_t)a.out_rows * row_bytes <= lim &&
                    (uint64_t)a.n_slots * (uint64_t)a.b * sizeof(double) <= lim;
-  const void *fn = stream_fn_for(t, buf, a.weights != nullptr, a.residual != 0);
-  if (!fn) return hipErrorInvalidValue;
-  if (a.chunk % kChunkQuantum != 0 || a.n % a.chunk != 0) return hipErrorInvalidValue;
+  const bool wt = a.weights != nullptr, res = a.residual != 0;
   const int64_t n_chunks = a.n / a.chunk;
-  const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
   StreamArgs arg = a;
   void *params[] = {&arg};
+  // B's column slice in LDS when it fits and two workgroups (24 waves) still
+  // fit a CU -- the variants with more registers (soft KB, residual hop at
+  // narrow rows) would drop below the register variant's four waves per SIMD
+  // and keep B in registers instead.  The grid is as many workgroups as the
+  // CUs hold at once, each copying the table once and walking its chunks
+  // grid-stride.
+  const size_t lds_bytes = (size_t)a.B_rows * (size_t)t.width * sizeof(float);
+  if (buf && o.b_in_lds && lds_bytes <= kMaxLdsB) {
+    const void *fn = stream_fn_for(t, true, true, wt, res);
+    if (!fn) return hipErrorInvalidValue;
+    const int per_cu = lds_blocks_per_cu(fn, lds_bytes);
+    if (per_cu >= 2) {
+      const int64_t cap = (int64_t)per_cu * (o.n_cu > 0 ? o.n_cu : 1);
+      const int64_t cap32 = cap > (int64_t)INT32_MAX ? (int64_t)INT32_MAX : cap;
+      const dim3 grid((unsigned)blocks_for(n_chunks, kBlockLds / t.lpt, (int)cap32),
+                      (unsigned)t.n_slices);
+      return hipLaunchKernel(fn, grid, dim3(kBlockLds), params, lds_bytes, s);
+    }
+  }
+  const void *fn = stream_fn_for(t, buf, false, wt, res);
+  if (!fn) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
   return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
 }
 

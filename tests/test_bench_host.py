@@ -65,9 +65,9 @@ def test_kernel_symbols_exist_in_the_build(bench):
     for b in (1, 4, 5, 32, 128, 256, 300):
         for weighted in (False, True):
             for residual in (False, True):
-                for plain in (False, True):
-                    sym = bench.stream_kernel_symbol(b, weighted, residual, plain)
-                    assert sym in digests, (b, weighted, residual, plain, sym)
+                for plain, lds in ((False, False), (False, True), (True, False)):
+                    sym = bench.stream_kernel_symbol(b, weighted, residual, plain, lds)
+                    assert sym in digests, (b, weighted, residual, plain, lds, sym)
 
 
 def test_committed_traffic_is_gated_by_the_fingerprint(bench, tmp_path, monkeypatch):

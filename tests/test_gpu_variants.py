@@ -2,8 +2,9 @@
 
 The stream kernel is instantiated per lane layout (4 floats per lane when
 b % 4 == 0, else 1; lane groups of 1..64 lanes; column slices beyond 256
-columns), per load path (raw buffer loads, or plain loads as for tables of
-4 GB or more), per hard or soft KB (App. A weights) and per plain or residual
+columns), per load path (raw buffer loads with the B table staged in LDS or
+with B rows held in registers, or plain loads as for tables of 4 GB or more),
+per hard or soft KB (App. A weights) and per plain or residual
 hop (Sec. 3.2, App. E).  Each combination runs forward and backward on a KB
 with 16-entry chunks (rows split over many chunks, deep combine trees, runs
 cut by chunk ends) and is compared elementwise with the oracle.
@@ -37,16 +38,19 @@ def small_kb(seed, n_e=300, n_r=7, n_t=6000):
     return s.astype(np.int32), r.astype(np.int32), o.astype(np.int32), n_e, n_r
 
 
-COMBOS = list(itertools.product([1, 4, 5, 36, 260], [False, True], [None, 0.5], [False, True]))
+COMBOS = list(itertools.product([1, 4, 5, 36, 260], [False, True], [None, 0.5],
+                                ["lds", "regs", "plain"]))
 
 
-@pytest.mark.parametrize("b,weighted,gamma,plain", COMBOS)
-def test_variant(kbf, b, weighted, gamma, plain, monkeypatch):
+@pytest.mark.parametrize("b,weighted,gamma,path", COMBOS)
+def test_variant(kbf, b, weighted, gamma, path, monkeypatch):
     monkeypatch.setenv("KBFOLLOW_CHUNK", "16")
     monkeypatch.setenv("KBFOLLOW_REL_CHUNK", "16")
     monkeypatch.setenv("KBFOLLOW_FAN_IN", "3")
-    if plain:
+    if path == "plain":
         monkeypatch.setenv("KBFOLLOW_PLAIN_LOADS", "1")
+    if path == "regs":
+        monkeypatch.setenv("KBFOLLOW_B_IN_LDS", "0")
     s, r, o, n_e, n_r = small_kb(b * 7 + weighted)
     g = np.random.default_rng(b)
     w = g.uniform(0.1, 2.0, len(s)).astype(np.float32) if weighted else None
@@ -63,7 +67,7 @@ def test_variant(kbf, b, weighted, gamma, plain, monkeypatch):
         wantY = oracle.follow_residual(s, r, o, n_e, n_r, X, R, gamma=gamma, weight=w)
         wantdX, wantdR = oracle.follow_backward_residual(s, r, o, n_e, n_r, X, R, dY,
                                                          gamma=gamma, weight=w)
-    label = f"b={b} weighted={weighted} gamma={gamma} plain={plain}"
+    label = f"b={b} weighted={weighted} gamma={gamma} path={path}"
     assert_close(Y, wantY, label + " Y")
     assert_close(from_em(dX), wantdX, label + " dX")
     assert_close(from_em(dR), wantdR, label + " dR")
