@@ -89,9 +89,9 @@ MAX_LDS_B = 80 * 1024  # largest B column slice the stream kernel stages in LDS
 
 def b_slice_fits_lds(b, b_rows):
     """Whether a pass's B table (b_rows rows; R for forward and dX, X for dR)
-    is small enough for the LDS variant.  The library also needs two of its
-    workgroups to fit a CU, which holds for the hard-KB, non-residual
-    variants at b >= 32."""
+    is small enough for the LDS variant.  The library also needs the LDS
+    variant to keep at least as many waves on a CU as the register variant,
+    which holds for the hard-KB, non-residual variants at b >= 32."""
     vec, lpt = column_tiling(b)
     return b_rows * vec * lpt * 4 <= MAX_LDS_B
 

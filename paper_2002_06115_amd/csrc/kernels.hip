@@ -586,10 +586,11 @@ const void *stream_fn_for(const ColumnTiling &t, bool buf, bool lds, bool wt, bo
              : stream_fn_sel<1, true, false>(t.lpt, wt, res);
 }
 
-// Workgroups of `fn` (kBlockLds threads, lds_bytes of dynamic LDS) that fit
+// Workgroups of `fn` (`block` threads, lds_bytes of dynamic LDS) that fit
 // one CU at once, from the runtime's occupancy calculator; cached per kernel
-// and LDS size.  0 when the query fails.
-int lds_blocks_per_cu(const void *fn, size_t lds_bytes) {
+// and LDS size (a kernel always launches with the same block).  0 when the
+// query fails.
+int blocks_per_cu(const void *fn, int block, size_t lds_bytes) {
   static std::mutex mu;
   static std::map<std::pair<const void *, size_t>, int> cache;
   std::lock_guard<std::mutex> lock(mu);
@@ -597,9 +598,9 @@ int lds_blocks_per_cu(const void *fn, size_t lds_bytes) {
   auto it = cache.find(key);
   if (it != cache.end()) return it->second;
   int n = 0;
-  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsB) !=
-          hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kBlockLds, lds_bytes) != hipSuccess) {
+  if ((lds_bytes > 0 && hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                            (int)kMaxLdsB) != hipSuccess) ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds_bytes) != hipSuccess) {
     (void)hipGetLastError();
     n = 0;
   }
@@ -671,18 +672,22 @@ hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_
   const int64_t n_chunks = a.n / a.chunk;
   StreamArgs arg = a;
   void *params[] = {&arg};
-  // B's column slice in LDS when it fits and two workgroups (24 waves) still
-  // fit a CU -- the variants with more registers (soft KB, residual hop at
-  // narrow rows) would drop below the register variant's four waves per SIMD
-  // and keep B in registers instead.  The grid is as many workgroups as the
-  // CUs hold at once, each copying the table once and walking its chunks
-  // grid-stride.
+  const void *reg_fn = stream_fn_for(t, buf, false, wt, res);
+  if (!reg_fn) return hipErrorInvalidValue;
+  // B's column slice in LDS when it fits and the LDS variant keeps at least
+  // as many waves on a CU as the register variant: where it needs more
+  // registers per lane than a 768-thread workgroup can be given twice (soft
+  // KB and residual hop at narrow rows), or where the register variant runs
+  // at eight waves per SIMD already (b = 1), B stays in registers.  The grid
+  // is as many workgroups as the CUs hold at once, each copying the table
+  // once and walking its chunks grid-stride.
   const size_t lds_bytes = (size_t)a.B_rows * (size_t)t.width * sizeof(float);
   if (buf && o.b_in_lds && lds_bytes <= kMaxLdsB) {
     const void *fn = stream_fn_for(t, true, true, wt, res);
     if (!fn) return hipErrorInvalidValue;
-    const int per_cu = lds_blocks_per_cu(fn, lds_bytes);
-    if (per_cu >= 2) {
+    const int per_cu = blocks_per_cu(fn, kBlockLds, lds_bytes);
+    const int reg_per_cu = blocks_per_cu(reg_fn, kBlock, 0);
+    if (per_cu > 0 && per_cu * kBlockLds >= reg_per_cu * kBlock) {
       const int64_t cap = (int64_t)per_cu * (o.n_cu > 0 ? o.n_cu : 1);
       const int64_t cap32 = cap > (int64_t)INT32_MAX ? (int64_t)INT32_MAX : cap;
       const dim3 grid((unsigned)blocks_for(n_chunks, kBlockLds / t.lpt, (int)cap32),
@@ -690,10 +695,8 @@ hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_
       return hipLaunchKernel(fn, grid, dim3(kBlockLds), params, lds_bytes, s);
     }
   }
-  const void *fn = stream_fn_for(t, buf, false, wt, res);
-  if (!fn) return hipErrorInvalidValue;
   const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
-  return hipLaunchKernel(fn, grid, dim3(kBlock), params, 0, s);
+  return hipLaunchKernel(reg_fn, grid, dim3(kBlock), params, 0, s);
 }
 
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int64_t n_slots,

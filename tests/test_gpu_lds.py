@@ -1,6 +1,7 @@
 """The stream kernel's two ways of reading the B operand: the whole column
-slice of B staged in LDS (used when it is at most 80 KB and two workgroups fit
-a CU), or one B row per run loaded into registers.  Both do the same FMAs in
+slice of B staged in LDS (used when it is at most 80 KB and the LDS variant
+keeps at least as many waves on a CU as the register variant), or one B row
+per run loaded into registers.  Both do the same FMAs in
 the same order, so their outputs must agree bit for bit, and both must match
 the oracle.  The KBs sit on either side of the 80 KB limit (R with 640 and 641
 rows at b = 32), include relation hubs split over many chunks, and cover the
