@@ -46,6 +46,9 @@ constexpr int kBlock = 256;   // threads per workgroup (4 wavefronts of 64)
 // fill a CU at the six waves per SIMD that the kernel's registers allow.
 constexpr int kBlockLds = 768;
 constexpr int kUnroll = 8;    // entries per step; a lane group keeps their loads in flight
+// The residual hop's empty-row fill: pieces per lane group, rows per batch.
+constexpr int kFillPieces = 4;
+constexpr int kFillBatch = 4;
 static_assert(kChunkQuantum % kUnroll == 0, "a chunk is a whole number of steps");
 
 // Buffer-resource word 3 for gfx9-family raw buffers, and an offset past any
@@ -507,18 +510,48 @@ __device__ __forceinline__ void zero_pieces(const int2 *__restrict__ pieces, int
       }
     }
   } else {
+    // gamma * res[row] into out[row].  A lane group takes kFillPieces
+    // consecutive pieces (every lane loads the same descriptors) and walks
+    // their rows as one flat sequence, kFillBatch rows at a time: all of a
+    // batch's row loads are issued before its stores, so the mostly one- or
+    // two-row pieces of a Zipf KB still keep many loads in flight.  (res may
+    // be out itself: each row is read and then written by the same lane.)
     if (c >= b) return;  // no barrier or shuffle below
-    const int64_t stride = n_blocks * GPB;
-    for (int64_t t = block * GPB + grp; t < n_pieces; t += stride) {
-      const int2 pc = pieces[t];  // first row, count
-      for (int i = 0; i < pc.y; ++i) {
-        const size_t off = (size_t)KBF_CHECKED((int64_t)pc.x + i, out_rows) * bb + c;
-        double y[VEC];
-        float r[VEC] = {};
-        if (res) load_row<VEC>(res + off, r);
+    const int64_t stride = n_blocks * GPB * kFillPieces;
+    for (int64_t t0 = (block * GPB + grp) * kFillPieces; t0 < n_pieces; t0 += stride) {
+      int first[kFillPieces], start[kFillPieces], end[kFillPieces];
+      int total = 0;
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) y[v] = 0.0 + (double)gamma * (double)r[v];
-        store_row<VEC>(out + off, y);
+      for (int j = 0; j < kFillPieces; ++j) {
+        const int2 pc = (t0 + j < n_pieces) ? pieces[t0 + j] : make_int2(0, 0);
+        first[j] = pc.x;
+        start[j] = total;
+        total += pc.y;
+        end[j] = total;
+      }
+      for (int k0 = 0; k0 < total; k0 += kFillBatch) {
+        int row[kFillBatch];
+        float r[kFillBatch][VEC];
+#pragma unroll
+        for (int u = 0; u < kFillBatch; ++u) {
+          const int k = k0 + u;
+          row[u] = -1;
+#pragma unroll
+          for (int j = 0; j < kFillPieces; ++j)
+            row[u] = (k >= start[j] && k < end[j]) ? first[j] + (k - start[j]) : row[u];
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) r[u][v] = 0.0f;
+          if (row[u] >= 0)
+            load_row<VEC>(res + (size_t)KBF_CHECKED((int64_t)row[u], out_rows) * bb + c, r[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kFillBatch; ++u) {
+          if (row[u] < 0) continue;
+          double y[VEC];
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) y[v] = 0.0 + (double)gamma * (double)r[u][v];
+          store_row<VEC>(out + (size_t)KBF_CHECKED((int64_t)row[u], out_rows) * bb + c, y);
+        }
       }
     }
   }
@@ -720,11 +753,12 @@ hipError_t launch_tail(const TailArgs &args, hipStream_t s) {
   if (!fn) return hipErrorInvalidValue;
   TailArgs a = args;
   // One combine task per lane group.  Empty rows, packed: LPT pieces per
-  // lane group, 256 per block; residual: one piece per lane group, so that
-  // each piece's rows are the only loads in front of their stores.
+  // lane group, 256 per block; residual: kFillPieces pieces per lane group.
   a.combine_blocks = a.n_tasks > 0 ? blocks_for(a.n_tasks, kBlock / t.lpt, 0) : 0;
   const int64_t zero_blocks =
-      a.n_pieces > 0 ? blocks_for(a.n_pieces, packed ? kBlock : kBlock / t.lpt, 0) : 0;
+      a.n_pieces > 0
+          ? blocks_for(a.n_pieces, packed ? kBlock : (kBlock / t.lpt) * kFillPieces, 0)
+          : 0;
   if (a.combine_blocks + zero_blocks > (int64_t)INT32_MAX) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(a.combine_blocks + zero_blocks), (unsigned)t.n_slices);
   void *params[] = {&a};
