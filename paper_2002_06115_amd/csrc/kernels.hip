@@ -241,8 +241,22 @@ __device__ __forceinline__ void store_row_buffer(__amdgpu_buffer_rsrc_t rsrc, ui
 // step's gathers are in flight, which leaves room for more waves per SIMD,
 // and the B reads leave the L2 alone.  Used when the table fits (R for the
 // forward and dX passes, at most kMaxLdsB bytes per slice).
+//
+// The residual-hop variant with B in LDS (4 floats per lane, 8 or more lanes
+// per group) needs 84 VGPRs, four more than six waves per SIMD allow; it is
+// compiled for six waves (80 VGPRs, a few registers spilled), which measured
+// faster than keeping B in registers (large KB forward 0.89 -> 0.84 ms).  The
+// same cap on the soft-KB variants or on narrower lane groups spilled inside
+// the loop and ran slower, so they keep the compiler's own allocation.
+template <int VEC, int LPT, bool WEIGHTED, bool RES, bool LDSB>
+constexpr int stream_min_waves() {
+  return (LDSB && RES && !WEIGHTED && VEC == 4 && LPT >= 8) ? 6 : 1;
+}
+
 template <int VEC, int LPT, bool BUF, bool WEIGHTED, bool RES, bool LDSB>
-__global__ __launch_bounds__(LDSB ? kBlockLds : kBlock) void stream_kernel(StreamArgs a) {
+__global__ __launch_bounds__((LDSB ? kBlockLds : kBlock),
+                             (stream_min_waves<VEC, LPT, WEIGHTED, RES, LDSB>())) void
+stream_kernel(StreamArgs a) {
   static_assert(BUF || !LDSB, "the LDS copy of B goes with raw buffer loads");
   constexpr int BLK = LDSB ? kBlockLds : kBlock;
   constexpr int GPB = BLK / LPT;
