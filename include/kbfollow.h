@@ -93,6 +93,10 @@ typedef enum {
  *   KBFOLLOW_FAN_IN                     partials per combine task (32);
  *   KBFOLLOW_PLAIN_LOADS=1              plain loads instead of raw buffer
  *                                       loads (bitwise the same);
+ *   KBFOLLOW_B_IN_LDS=0                 the second operand (R, or X for dR)
+ *                                       read into registers per run even
+ *                                       where its table fits LDS (bitwise
+ *                                       the same);
  *   KBFOLLOW_LAYOUT_SORT=counting       the chained counting sorts for
  *                                       every KB (bitwise the same).
  */
