@@ -76,10 +76,10 @@ def pass_bytes(kb, b, phase, whole_pass=False):
 
 def column_tiling(b):
     """(VEC, LPT): 4 floats per lane when b % 4 == 0 (else 1), lanes per group
-    b / VEC rounded up to a power of two, at most 64."""
+    b / VEC rounded up to a power of two, at most 32."""
     vec = 4 if b % 4 == 0 else 1
     lanes, lpt = -(-b // vec), 1
-    while lpt < lanes and lpt < 64:
+    while lpt < lanes and lpt < 32:
         lpt *= 2
     return vec, lpt
 

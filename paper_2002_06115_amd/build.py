@@ -99,7 +99,9 @@ def build_probe(verbose: bool = False) -> str:
 def fingerprint(defines, path, bdir, csrc=CSRC) -> dict:
     """Per-kernel sha256 of the gfx950 assembly of kernels.hip, written as JSON
     {mangled kernel name: digest}: identifies the device code that rocprofv3
-    counters were taken on (compiler-unique ids and debug lines excluded)."""
+    counters were taken on (compiler-unique ids, debug lines and the numbering
+    of basic-block labels, which depends on the kernel's place in the file,
+    excluded)."""
     import hashlib
     import json
     import re
@@ -109,6 +111,7 @@ def fingerprint(defines, path, bdir, csrc=CSRC) -> dict:
     subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
     digests, name, h = {}, None, None
     start = re.compile(r"^(_Z\S+):\s*(;.*)?$")
+    bb_label = re.compile(r"BB\d+_")  # .LBB<function>_<block>, also in comments
     with open(asm) as f:
         for line in f:
             m = start.match(line)
@@ -120,7 +123,7 @@ def fingerprint(defines, path, bdir, csrc=CSRC) -> dict:
                     digests[name] = h.hexdigest()
                     name = None
                 elif "__hip_cuid" not in line and not line.lstrip().startswith((".loc", ".file")):
-                    h.update(line.encode())
+                    h.update(bb_label.sub("BB_", line).encode())
     with open(path, "w") as f:
         json.dump(digests, f, indent=0, sort_keys=True)
     return digests

@@ -11,7 +11,7 @@ namespace kbf {
 // How the columns of a b-wide row are spread over the lanes of a lane group.
 struct ColumnTiling {
   int vec;       // floats per lane per access: 4 (b % 4 == 0) or 1
-  int lpt;       // lanes per group (power of two, <= 64): one group walks one chunk
+  int lpt;       // lanes per group (power of two, <= 32): one group walks one chunk
   int width;     // columns one group covers, lpt * vec
   int n_slices;  // ceil(b / width): grid y dimension
 };

@@ -1,7 +1,7 @@
 """Every kernel variant against the oracle.
 
 The stream kernel is instantiated per lane layout (4 floats per lane when
-b % 4 == 0, else 1; lane groups of 1..64 lanes; column slices beyond 256
+b % 4 == 0, else 1; lane groups of 1..32 lanes; column slices beyond 128
 columns), per load path (raw buffer loads with the B table staged in LDS or
 with B rows held in registers, or plain loads as for tables of 4 GB or more),
 per hard or soft KB (App. A weights) and per plain or residual
