@@ -84,23 +84,35 @@ def column_tiling(b):
     return vec, lpt
 
 
-MAX_LDS_B = 80 * 1024  # largest B column slice the stream kernel stages in LDS
+MAX_LDS_B = 80 * 1024     # B slice staged in LDS with two workgroups per CU
+MAX_LDS_BIG = 160 * 1024  # with one workgroup per CU (hard KB only)
 
 
-def b_slice_fits_lds(b, b_rows):
-    """Whether a pass's B table (b_rows rows; R for forward and dX, X for dR)
-    is small enough for the LDS variant.  The library also needs the LDS
-    variant to keep at least as many waves on a CU as the register variant,
-    which holds for the hard-KB, non-residual variants at b >= 32."""
+def stream_launch(b, b_rows, hard=True):
+    """(LPT, lds) of the stream kernel a pass launches for batch b when its B
+    table has b_rows rows (R for forward and dX, X for dR): B in LDS when its
+    column slice fits (hard KB: rows cut into 32-column slices where that
+    makes it fit).  The library also needs the LDS variant to keep at least as
+    many waves on a CU as the register variant, which holds for the hard-KB,
+    non-residual variants at b >= 32."""
     vec, lpt = column_tiling(b)
-    return b_rows * vec * lpt * 4 <= MAX_LDS_B
+    if b_rows * vec * lpt * 4 <= MAX_LDS_B:
+        return lpt, True
+    if not hard:
+        return lpt, False
+    narrow = 8 if vec == 4 and lpt > 8 else lpt
+    if b_rows * vec * narrow * 4 <= MAX_LDS_BIG:
+        return narrow, True
+    return lpt, False
 
 
-def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False, lds=False):
+def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False, lds=False,
+                         lpt=None):
     """Mangled name of the stream-kernel instance a pass launches for batch b:
-    lane layout from column_tiling, raw-buffer loads unless a table reaches
-    4 GB, B staged in LDS (lds) or held in registers."""
-    vec, lpt = column_tiling(b)
+    lane layout from column_tiling (or lpt lanes per group), raw-buffer loads
+    unless a table reaches 4 GB, B staged in LDS (lds) or held in registers."""
+    vec, lpt0 = column_tiling(b)
+    lpt = lpt or lpt0
     flag = lambda v: 1 if v else 0
     return (f"_ZN3kbf12_GLOBAL__N_113stream_kernelILi{vec}ELi{lpt}ELb{flag(not plain_loads)}"
             f"ELb{flag(weighted)}ELb{flag(residual)}ELb{flag(lds and not plain_loads)}"
@@ -514,10 +526,12 @@ def main():
         gather_b, comp_b, once_b = pass_bytes(kb, b, dom)
         sec = ms_avg * 1e-3
         b_rows = w.n_entities if dom == "dr_stream" else w.n_relations
+        lpt, lds = stream_launch(b, b_rows, hard=args.residual is None)
+        if os.environ.get("KBFOLLOW_B_IN_LDS") == "0":
+            lpt, lds = None, False
         symbol = stream_kernel_symbol(b, residual=args.residual is not None,
                                       plain_loads=os.environ.get("KBFOLLOW_PLAIN_LOADS") == "1",
-                                      lds=os.environ.get("KBFOLLOW_B_IN_LDS") != "0"
-                                      and b_slice_fits_lds(b, b_rows))
+                                      lds=lds, lpt=lpt)
         traffic = measured_traffic(w.name, b, dom, symbol)
         roof = {"bound": "hbm", "achieved": round(comp_b / sec / 1e9, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(comp_b / sec / 1e9 / PEAK_HBM_GBPS, 4),

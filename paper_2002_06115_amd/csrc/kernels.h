@@ -16,6 +16,8 @@ struct ColumnTiling {
   int n_slices;  // ceil(b / width): grid y dimension
 };
 ColumnTiling column_tiling(int32_t b);
+// The same with lane groups of at most max_lpt lanes (a power of two <= 32).
+ColumnTiling column_tiling_max(int32_t b, int max_lpt);
 
 // Chunk lengths must be multiples of this (the kernel's step, kUnroll entries).
 constexpr int32_t kChunkQuantum = 8;
@@ -54,15 +56,17 @@ struct StreamArgs {
   const float *Z;  // the rows added at markers when residual is set
 };
 // Largest B column slice (B_rows * slice width * 4 bytes) the stream kernel
-// copies into LDS: two copies fit a CU's 160 KB.
+// copies into LDS with two workgroups per CU (two copies fit a CU's 160 KB),
+// and with one workgroup per CU (hard KB only).
 constexpr size_t kMaxLdsB = 80 * 1024;
+constexpr size_t kMaxLdsBig = 160 * 1024;
 
 struct StreamOptions {
   // Forces the plain-load variant (used anyway for tables of 4 GB or more)
   // so it can be tested at small sizes.
   bool plain_loads = false;
-  // Stage B in LDS when its slice fits kMaxLdsB (raw-buffer path only);
-  // off keeps B rows in registers, the variant used for larger tables.
+  // Stage B in LDS when its slice fits (raw-buffer path only); off keeps B
+  // rows in registers, the variant used for larger tables.
   bool b_in_lds = true;
   int n_cu = 1;  // compute units of the device, for the LDS variant's grid
 };

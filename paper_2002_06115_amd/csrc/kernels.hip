@@ -33,6 +33,7 @@
 
 #include <climits>
 #include <map>
+#include <tuple>
 #include <mutex>
 #include <utility>
 
@@ -42,10 +43,13 @@ namespace {
 
 constexpr int kBlock = 256;   // threads per workgroup (4 wavefronts of 64)
 constexpr int kMaxLpt = 32;   // widest lane group (column_tiling)
-// Workgroup of the stream kernel when the B table sits in LDS: 12 waves, so
-// that two workgroups (two copies of the table, up to kMaxLdsB bytes each)
-// fill a CU at the six waves per SIMD that the kernel's registers allow.
+// Workgroups of the stream kernel when the B table sits in LDS: 12 waves,
+// so that two workgroups (two copies of a table of up to kMaxLdsB bytes) fill
+// a CU at the six waves per SIMD that the kernel's registers allow; 16 waves,
+// one workgroup per CU, for a table of up to kMaxLdsBig bytes.  The LDS
+// variants are compiled for the larger block and read blockDim at run time.
 constexpr int kBlockLds = 768;
+constexpr int kBlockLdsBig = 1024;
 constexpr int kUnroll = 8;    // entries per step; a lane group keeps their loads in flight
 // The residual hop's empty-row fill: pieces per lane group, rows per batch.
 constexpr int kFillPieces = 4;
@@ -254,12 +258,12 @@ constexpr int stream_min_waves() {
 }
 
 template <int VEC, int LPT, bool BUF, bool WEIGHTED, bool RES, bool LDSB>
-__global__ __launch_bounds__((LDSB ? kBlockLds : kBlock),
+__global__ __launch_bounds__((LDSB ? kBlockLdsBig : kBlock),
                              (stream_min_waves<VEC, LPT, WEIGHTED, RES, LDSB>())) void
 stream_kernel(StreamArgs a) {
   static_assert(BUF || !LDSB, "the LDS copy of B goes with raw buffer loads");
-  constexpr int BLK = LDSB ? kBlockLds : kBlock;
-  constexpr int GPB = BLK / LPT;
+  const int BLK = LDSB ? (int)blockDim.x : kBlock;  // kBlockLds or kBlockLdsBig
+  const int GPB = BLK / LPT;
   constexpr int W = LPT * VEC;  // columns of one slice
   extern __shared__ float b_lds[];  // [B_rows][W] with LDSB
   const int lane = threadIdx.x % LPT;
@@ -633,19 +637,18 @@ const void *stream_fn_for(const ColumnTiling &t, bool buf, bool lds, bool wt, bo
 }
 
 // Workgroups of `fn` (`block` threads, lds_bytes of dynamic LDS) that fit
-// one CU at once, from the runtime's occupancy calculator; cached per kernel
-// and LDS size (a kernel always launches with the same block).  0 when the
-// query fails.
+// one CU at once, from the runtime's occupancy calculator; cached per kernel,
+// block and LDS size.  0 when the query fails.
 int blocks_per_cu(const void *fn, int block, size_t lds_bytes) {
   static std::mutex mu;
-  static std::map<std::pair<const void *, size_t>, int> cache;
+  static std::map<std::tuple<const void *, int, size_t>, int> cache;
   std::lock_guard<std::mutex> lock(mu);
-  const auto key = std::make_pair(fn, lds_bytes);
+  const auto key = std::make_tuple(fn, block, lds_bytes);
   auto it = cache.find(key);
   if (it != cache.end()) return it->second;
   int n = 0;
   if ((lds_bytes > 0 && hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                            (int)kMaxLdsB) != hipSuccess) ||
+                                            (int)kMaxLdsBig) != hipSuccess) ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, block, lds_bytes) != hipSuccess) {
     (void)hipGetLastError();
     n = 0;
@@ -689,7 +692,9 @@ int64_t blocks_for(int64_t items, int per_block, int max_blocks) {
 
 }  // namespace
 
-ColumnTiling column_tiling(int32_t b) {
+ColumnTiling column_tiling(int32_t b) { return column_tiling_max(b, kMaxLpt); }
+
+ColumnTiling column_tiling_max(int32_t b, int max_lpt) {
   ColumnTiling t;
   t.vec = (b % 4 == 0) ? 4 : 1;
   const int lanes = (b + t.vec - 1) / t.vec;
@@ -700,7 +705,7 @@ ColumnTiling column_tiling(int32_t b) {
   // Infinity Cache: at b = 256 on a 2 M-entity KB, 64-lane groups took
   // 4.02 / 4.03 ms for the dX / dR passes, two 32-lane slices 3.71 / 3.82.
   int lpt = 1;
-  while (lpt < lanes && lpt < kMaxLpt) lpt <<= 1;
+  while (lpt < lanes && lpt < max_lpt) lpt <<= 1;
   t.lpt = lpt;
   t.width = lpt * t.vec;
   t.n_slices = (b + t.width - 1) / t.width;
@@ -726,23 +731,36 @@ hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_
   if (!reg_fn) return hipErrorInvalidValue;
   // B's column slice in LDS when it fits and the LDS variant keeps at least
   // as many waves on a CU as the register variant: where it needs more
-  // registers per lane than a 768-thread workgroup can be given twice (soft
-  // KB and residual hop at narrow rows), or where the register variant runs
-  // at eight waves per SIMD already (b = 1), B stays in registers.  The grid
-  // is as many workgroups as the CUs hold at once, each copying the table
-  // once and walking its chunks grid-stride.
-  const size_t lds_bytes = (size_t)a.B_rows * (size_t)t.width * sizeof(float);
-  if (buf && o.b_in_lds && lds_bytes <= kMaxLdsB) {
-    const void *fn = stream_fn_for(t, true, true, wt, res);
-    if (!fn) return hipErrorInvalidValue;
-    const int per_cu = blocks_per_cu(fn, kBlockLds, lds_bytes);
-    const int reg_per_cu = blocks_per_cu(reg_fn, kBlock, 0);
-    if (per_cu > 0 && per_cu * kBlockLds >= reg_per_cu * kBlock) {
-      const int64_t cap = (int64_t)per_cu * (o.n_cu > 0 ? o.n_cu : 1);
-      const int64_t cap32 = cap > (int64_t)INT32_MAX ? (int64_t)INT32_MAX : cap;
-      const dim3 grid((unsigned)blocks_for(n_chunks, kBlockLds / t.lpt, (int)cap32),
-                      (unsigned)t.n_slices);
-      return hipLaunchKernel(fn, grid, dim3(kBlockLds), params, lds_bytes, s);
+  // registers per lane than its workgroup can be given (b = 4 .. 16, the
+  // soft KB), or where the register variant runs at eight waves per SIMD
+  // already (b = 1), B stays in registers.  A slice of at most kMaxLdsB bytes
+  // goes with two 768-thread workgroups per CU; for the hard KB a slice of up
+  // to kMaxLdsBig bytes goes with one 1024-thread workgroup, and rows wider
+  // than 32 columns whose slice is too large are cut into 32-column slices
+  // (one 128-byte line of every row each) when that makes B fit.  The grid
+  // is as many workgroups as the CUs hold at once, each copying its slice of
+  // the table once and walking its chunks grid-stride.
+  if (buf && o.b_in_lds) {
+    const bool hard = !wt && !res;
+    ColumnTiling tl = t;
+    size_t lds_bytes = (size_t)a.B_rows * (size_t)tl.width * sizeof(float);
+    if (hard && lds_bytes > kMaxLdsB && t.vec == 4 && t.width > 32) {
+      tl = column_tiling_max(a.b, 8);
+      lds_bytes = (size_t)a.B_rows * (size_t)tl.width * sizeof(float);
+    }
+    const int blk = lds_bytes <= kMaxLdsB ? kBlockLds : kBlockLdsBig;
+    if (lds_bytes <= (hard ? kMaxLdsBig : kMaxLdsB)) {
+      const void *fn = stream_fn_for(tl, true, true, wt, res);
+      if (!fn) return hipErrorInvalidValue;
+      const int per_cu = blocks_per_cu(fn, blk, lds_bytes);
+      const int reg_per_cu = blocks_per_cu(reg_fn, kBlock, 0);
+      if (per_cu > 0 && per_cu * blk >= reg_per_cu * kBlock) {
+        const int64_t cap = (int64_t)per_cu * (o.n_cu > 0 ? o.n_cu : 1);
+        const int64_t cap32 = cap > (int64_t)INT32_MAX ? (int64_t)INT32_MAX : cap;
+        const dim3 grid((unsigned)blocks_for(n_chunks, blk / tl.lpt, (int)cap32),
+                        (unsigned)tl.n_slices);
+        return hipLaunchKernel(fn, grid, dim3(blk), params, lds_bytes, s);
+      }
     }
   }
   const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);

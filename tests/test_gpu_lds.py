@@ -1,11 +1,15 @@
 """The stream kernel's two ways of reading the B operand: the whole column
-slice of B staged in LDS (used when it is at most 80 KB and the LDS variant
-keeps at least as many waves on a CU as the register variant), or one B row
-per run loaded into registers.  Both do the same FMAs in
-the same order, so their outputs must agree bit for bit, and both must match
-the oracle.  The KBs sit on either side of the 80 KB limit (R with 640 and 641
-rows at b = 32), include relation hubs split over many chunks, and cover the
-dR pass of a small-entity KB whose B table (X) fits LDS too."""
+slice of B staged in LDS (up to 80 KB with two workgroups per CU, up to 160 KB
+with one for the hard KB, rows cut into 32-column slices where that makes B
+fit; used when the LDS variant keeps at least as many waves on a CU as the
+register variant), or one B row per run loaded into registers.  Both do the
+same FMAs in the same order, so their outputs must agree bit for bit, and
+both must match the oracle.  The KBs sit on either side of the 80 KB and
+160 KB limits (R with 640 / 641 and 1280 / 1281 rows at b = 32), need the
+32-column slices (b = 128 with 161 relations, b = 256 with 1000, b = 260 with
+700: nine slices, the last four columns wide), include relation hubs split
+over many chunks, and cover the dR pass of a small-entity KB whose B table
+(X) fits LDS too."""
 import numpy as np
 import pytest
 
@@ -43,8 +47,9 @@ def run(kbf, monkeypatch, lds, s, r, o, n_e, n_r, X, R, dY, weight=None, gamma=N
     return out
 
 
-@pytest.mark.parametrize("b,n_r", [(32, 640), (32, 641), (128, 160), (128, 161), (5, 300),
-                                   (1, 2000), (256, 80), (260, 40)])
+@pytest.mark.parametrize("b,n_r", [(32, 640), (32, 641), (32, 1280), (32, 1281), (128, 160),
+                                   (128, 161), (5, 300), (1, 2000), (256, 80), (256, 1000),
+                                   (260, 40), (260, 700)])
 def test_lds_and_register_paths_agree(kbf, monkeypatch, b, n_r):
     monkeypatch.setenv("KBFOLLOW_CHUNK", "32")
     n_e, n_t = 5000, 60_000
