@@ -103,3 +103,30 @@ def test_residual_chain_replay(kbf):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(bits(xs[3]), bits(want)), f"replay {i}"
+
+
+def test_first_launch_under_capture(kbf):
+    """The launcher's first call for a kernel and LDS size queries the
+    occupancy calculator and sets the kernel's LDS limit; when that first call
+    is being captured, the graph must still replay correctly.  (37 relations
+    at b = 32 give an LDS size no other test uses.)"""
+    import torch
+    rng = np.random.default_rng(37)
+    n_e, n_r, n_t, b = 3000, 37, 30_000, 32
+    s = rng.integers(0, n_e, n_t).astype(np.int32)
+    r = rng.integers(0, n_r, n_t).astype(np.int32)
+    o = rng.integers(0, n_e, n_t).astype(np.int32)
+    gkb = kbf.KB(s, r, o, n_e, n_r)
+    X = to_em(rng.standard_normal((b, n_e)).astype(np.float32))
+    R = to_em(rng.standard_normal((b, n_r)).astype(np.float32))
+    Y = torch.empty_like(X)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        gkb.follow(X, R, out=Y)
+    for i in range(3):
+        Y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        want = gkb.follow(X, R)
+        torch.cuda.synchronize()
+        assert torch.equal(bits(Y), bits(want)), f"replay {i}"
