@@ -104,3 +104,20 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0 and "one GPU" in r.stderr
+
+
+def test_stream_launch_mirrors_the_library_rule(bench):
+    """bench.stream_launch: (lanes per group, B in LDS) for a pass whose B
+    table has b_rows rows, as the library's launcher chooses it for the hard
+    KB: the default layout when B's slice fits 80 KB, 32-column slices when
+    that makes it fit 160 KB, registers otherwise."""
+    assert bench.stream_launch(32, 600) == (8, True)        # 76.8 KB
+    assert bench.stream_launch(32, 1280) == (8, True)       # 160 KB, one workgroup per CU
+    assert bench.stream_launch(32, 1281) == (8, False)
+    assert bench.stream_launch(128, 160) == (32, True)      # 80 KB at 128 columns
+    assert bench.stream_launch(128, 161) == (8, True)       # cut into 32-column slices
+    assert bench.stream_launch(256, 1000) == (8, True)      # 128 KB per 32-column slice
+    assert bench.stream_launch(256, 10_000_000) == (32, False)
+    assert bench.stream_launch(256, 1000, hard=False) == (32, False)
+    assert bench.stream_kernel_symbol(256, lds=True, lpt=8) == \
+        "_ZN3kbf12_GLOBAL__N_113stream_kernelILi4ELi8ELb1ELb0ELb0ELb1EEEvNS_10StreamArgsE"
