@@ -244,7 +244,8 @@ __device__ __forceinline__ void store_row_buffer(__amdgpu_buffer_rsrc_t rsrc, ui
 // there when the FMAs need it.  No B row is then held in registers while a
 // step's gathers are in flight, which leaves room for more waves per SIMD,
 // and the B reads leave the L2 alone.  Used when the table fits (R for the
-// forward and dX passes, at most kMaxLdsB bytes per slice).
+// forward and dX passes: at most kMaxLdsB bytes per slice with 768-thread
+// workgroups, kMaxLdsBig with 1024; see launch_stream).
 //
 // The residual-hop variant with B in LDS (4 floats per lane, 8 or more lanes
 // per group) needs 84 VGPRs, four more than six waves per SIMD allow; it is
