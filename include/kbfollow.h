@@ -81,7 +81,8 @@ typedef enum {
  * weights) plus about 8 bytes per non-empty row per layout.  Building sorts
  * the triples three ways (radix sorts of one 64-bit key per triple when
  * 2 * bits(N_E - 1) + bits(N_R - 1) <= 64, else chained counting sorts) on
- * up to three host threads.
+ * up to 16 host threads (the calling thread plus threads it starts and joins
+ * before returning).
  * Errors: KB_EINVAL (sizes, null pointers), KB_ERANGE (an id out of range;
  * checked before any device work), KB_ENOMEM, KB_EHIP.
  *
@@ -98,7 +99,10 @@ typedef enum {
  *                                       where its table fits LDS (bitwise
  *                                       the same);
  *   KBFOLLOW_LAYOUT_SORT=counting       the chained counting sorts for
- *                                       every KB (bitwise the same).
+ *                                       every KB (bitwise the same);
+ *   KBFOLLOW_HOST_THREADS               host threads for the layout sorts
+ *                                       (default: the hardware's, at most 16;
+ *                                       the same layouts for any count).
  */
 kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                     const int32_t *subj, const int32_t *rel, const int32_t *obj,

@@ -14,6 +14,7 @@
 #include "plan.h"
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstdio>
 #include <exception>
 #include <thread>
@@ -98,43 +99,93 @@ static void fill_layout(LayoutHost &L, int64_t rows, std::vector<int32_t> &&orde
 }
 
 // Stable LSD radix sort of `key` (11-bit digits, as many passes as the
-// largest key has digits; all digit histograms from one read), carrying the
-// triple ids along when `id` is non-null.  Each pass is a sequential read and
-// a scatter into 2048 buckets, unlike a counting sort over an id space of
-// millions, whose gathers and scatters miss the caches.
-static void radix_sort(std::vector<uint64_t> &key, std::vector<int32_t> *id) {
+// largest key has digits), carrying the triple ids along when `id` is
+// non-null, on `threads` host threads.  Each pass: every thread counts the
+// digits of its contiguous block of the input; the bucket of digit d for
+// thread t starts after all smaller digits and after digit d of the threads
+// before t, so each thread scatters its block in order and the pass is
+// stable, whatever the thread count (the result is the same for any).  A pass
+// is a sequential read and a scatter into 2048 buckets, unlike a counting
+// sort over an id space of millions, whose gathers and scatters miss the
+// caches.
+static void radix_sort(std::vector<uint64_t> &key, std::vector<int32_t> *id, int threads) {
   constexpr int kBits = 11, kDigits = 1 << kBits, kMaxPasses = (64 + kBits - 1) / kBits;
   const int64_t n = (int64_t)key.size();
+  if (n == 0) return;
+  const int T = (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)threads, n / 65536 + 1, 64}));
+  auto run = [T](auto &&fn) {  // fn(t) for t in [0, T), on T threads
+    std::vector<std::thread> pool;
+    std::exception_ptr err[64];
+    for (int t = 1; t < T; ++t)
+      pool.emplace_back([&, t] {
+        try {
+          fn(t);
+        } catch (...) {
+          err[t] = std::current_exception();
+        }
+      });
+    try {
+      fn(0);
+    } catch (...) {
+      err[0] = std::current_exception();
+    }
+    for (auto &th : pool) th.join();
+    for (int t = 0; t < T; ++t)
+      if (err[t]) std::rethrow_exception(err[t]);
+  };
+  auto lo = [n, T](int t) { return n * t / T; };
+  // Which digits occur at all: passes beyond the largest key's top digit are
+  // skipped.
+  std::vector<uint64_t> any_t(T, 0);
+  run([&](int t) {
+    uint64_t a = 0;
+    for (int64_t i = lo(t); i < lo(t + 1); ++i) a |= key[i];
+    any_t[t] = a;
+  });
   uint64_t any = 0;
-  for (uint64_t k : key) any |= k;
+  for (uint64_t a : any_t) any |= a;
   int passes = 0;
   while (passes < kMaxPasses && (any >> (passes * kBits)) != 0) ++passes;
-  std::vector<int64_t> count((size_t)passes * kDigits, 0);
-  for (uint64_t k : key)
-    for (int q = 0; q < passes; ++q) ++count[(size_t)q * kDigits + ((k >> (q * kBits)) & (kDigits - 1))];
   std::vector<uint64_t> key2(n);
   std::vector<int32_t> id2(id ? n : 0);
+  std::vector<int64_t> count((size_t)T * kDigits);
   for (int q = 0; q < passes; ++q) {
-    int64_t *c = count.data() + (size_t)q * kDigits;
-    if (*std::max_element(c, c + kDigits) == n) continue;  // one digit value: order unchanged
-    int64_t sum = 0;
-    for (int d = 0; d < kDigits; ++d) {
-      const int64_t t = c[d];
-      c[d] = sum;
-      sum += t;
-    }
     const int shift = q * kBits;
-    if (id) {
-      for (int64_t i = 0; i < n; ++i) {
-        const int64_t p = c[(key[i] >> shift) & (kDigits - 1)]++;
-        key2[p] = key[i];
-        id2[p] = (*id)[i];
-      }
-      id->swap(id2);
-    } else {
-      for (int64_t i = 0; i < n; ++i) key2[c[(key[i] >> shift) & (kDigits - 1)]++] = key[i];
+    run([&](int t) {
+      int64_t *c = count.data() + (size_t)t * kDigits;
+      std::fill(c, c + kDigits, 0);
+      for (int64_t i = lo(t); i < lo(t + 1); ++i) ++c[(key[i] >> shift) & (kDigits - 1)];
+    });
+    // One digit value for every key: the order is unchanged.
+    bool single = false;
+    for (int d = 0; d < kDigits && !single; ++d) {
+      int64_t tot = 0;
+      for (int t = 0; t < T; ++t) tot += count[(size_t)t * kDigits + d];
+      single = tot == n;
     }
+    if (single) continue;
+    int64_t sum = 0;
+    for (int d = 0; d < kDigits; ++d)
+      for (int t = 0; t < T; ++t) {
+        int64_t &c = count[(size_t)t * kDigits + d];
+        const int64_t v = c;
+        c = sum;
+        sum += v;
+      }
+    run([&](int t) {
+      int64_t *c = count.data() + (size_t)t * kDigits;
+      if (id) {
+        for (int64_t i = lo(t); i < lo(t + 1); ++i) {
+          const int64_t p = c[(key[i] >> shift) & (kDigits - 1)]++;
+          key2[p] = key[i];
+          id2[p] = (*id)[i];
+        }
+      } else {
+        for (int64_t i = lo(t); i < lo(t + 1); ++i) key2[c[(key[i] >> shift) & (kDigits - 1)]++] = key[i];
+      }
+    });
     key.swap(key2);
+    if (id) id->swap(id2);
   }
 }
 
@@ -149,6 +200,17 @@ static std::vector<int32_t> offsets_of(const std::vector<int32_t> &row, int64_t 
     off[k] = (int32_t)p;
   }
   return off;
+}
+
+// Host threads the layout build may use: the hardware's count, at most 16
+// (a GPU machine's CPU share), or KBFOLLOW_HOST_THREADS when set (>= 1).
+static int host_threads() {
+  if (const char *v = std::getenv("KBFOLLOW_HOST_THREADS")) {
+    const int n = std::atoi(v);
+    if (n >= 1) return std::min(n, 64);
+  }
+  const unsigned hw = std::thread::hardware_concurrency();
+  return (int)std::max(1u, std::min(hw, 16u));
 }
 
 void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
@@ -173,6 +235,11 @@ void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     // keys, and the triple ids are carried along only for the weights and
     // the permutation.
     const bool need_id = weight != nullptr || keep_perm;
+    // Host threads: the three orders run side by side (while their scratch
+    // stays modest) and each radix sort splits its passes over its share.
+    const int budget = host_threads();
+    const bool side_by_side = n_triples <= (int64_t(1) << 27);
+    const int sort_threads = side_by_side ? std::max(1, budget / 3) : budget;
     auto one = [&](int which) {
       const int64_t n = n_triples;
       std::vector<uint64_t> key(n);
@@ -196,7 +263,7 @@ void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
         ids.resize(n);
         for (int64_t l = 0; l < n; ++l) ids[l] = (int32_t)l;
       }
-      radix_sort(key, need_id ? &ids : nullptr);
+      radix_sort(key, need_id ? &ids : nullptr, sort_threads);
       LayoutHost &L = out[which];
       L.rows = rows;
       L.row.resize(n);
@@ -217,7 +284,7 @@ void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
       if (keep_offsets) L.offsets = offsets_of(L.row, rows);
       if (keep_perm) L.perm = std::move(ids);
     };
-    const bool parallel = n_triples <= (int64_t(1) << 27);
+    const bool parallel = side_by_side;
     if (!parallel) {
       for (int which : {BY_OBJ, BY_SUBJ, BY_REL}) one(which);
       return;

@@ -119,3 +119,20 @@ def test_product_path_has_no_cpu_fallback():
     src = open(os.path.join(ROOT, "paper_2002_06115_amd", "__init__.py")).read()
     assert "oracle" not in src.replace("oracle.", "")  # no import of the oracle package
     assert "import oracle" not in src and "from oracle" not in src
+
+
+@pytest.mark.parametrize("threads", ["1", "2", "5", "16"])
+def test_layout_sort_same_for_any_thread_count(kbf, threads, monkeypatch):
+    """The radix sorts split each pass over host threads (contiguous blocks,
+    per-thread digit buckets): the order must be the stable (k1, k2, k3) order
+    whatever the thread count.  300 k triples: several blocks per pass."""
+    monkeypatch.setenv("KBFOLLOW_HOST_THREADS", threads)
+    g = np.random.default_rng(17)
+    n_e, n_r, n_t = 50_000, 40, 300_000
+    s = np.minimum(g.zipf(1.3, n_t) - 1, n_e - 1).astype(np.int32)
+    r = g.integers(0, n_r, n_t).astype(np.int32)
+    o = g.integers(0, n_e, n_t).astype(np.int32)
+    specs = {0: (o, r, s), 1: (s, r, o), 2: (r, s, o)}
+    for which, (k1, k2, k3) in specs.items():
+        off, ca, cb, perm = kbf.layout_host(s, r, o, n_e, n_r, which)
+        assert np.array_equal(perm, np.lexsort((np.arange(n_t), k3, k2, k1))), which
