@@ -29,7 +29,11 @@
  * Streams: every compute call only enqueues work on `stream` (a hipStream_t;
  * NULL = the null stream) and returns; it never synchronises the host and
  * never allocates device memory.  Scratch space comes from the caller's
- * `workspace`, sized with kb_workspace_size().
+ * `workspace`, sized with kb_workspace_size().  On KBs of 2^20 triples or
+ * more, kb_follow_backward runs its dR pass on a stream the KB owns, forked
+ * from `stream` with an event and joined back into it before returning, so
+ * that work enqueued on `stream` afterwards still follows both passes (and
+ * a graph captured on `stream` contains both).
  *
  * Errors: argument checks run on the host before anything is enqueued; on
  * failure nothing is launched and no output is touched.  The status says what
@@ -100,6 +104,9 @@ typedef enum {
  *                                       the same);
  *   KBFOLLOW_LAYOUT_SORT=counting       the chained counting sorts for
  *                                       every KB (bitwise the same);
+ *   KBFOLLOW_OVERLAP_BACKWARD=0|1       dR concurrent with dX on the KB's
+ *                                       own stream (default: from 2^20
+ *                                       triples; bitwise the same);
  *   KBFOLLOW_HOST_THREADS               host threads for the layout sorts
  *                                       (default: the hardware's, at most 16;
  *                                       the same layouts for any count).
@@ -150,7 +157,8 @@ kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, f
  *   dR       : DEVICE float [N_R][b], overwritten, or NULL to skip it.
  *   Outputs must not overlap each other or any input, and the workspace
  *   overlaps none of the arrays.  Workspace and stream as for kb_follow (dX
- *   and dR reuse the same workspace one after the other).
+ *   and dR use disjoint parts of the workspace, since on a large KB the two
+ *   passes run concurrently; see Streams above).
  */
 kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const float *R,
                              const float *dY, float *dX, float *dR, void *workspace,

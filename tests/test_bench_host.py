@@ -95,9 +95,15 @@ def test_committed_profiles_match_the_built_kernels(bench):
     fp = os.path.join(ROOT, "paper_2002_06115_amd", "_lib", "kernels.fingerprint")
     if not os.path.exists(fp):
         pytest.skip("run __graft_entry__.build() first")
-    for workload, b in (("large", 32), ("train", 256)):
-        sym = bench.stream_kernel_symbol(b)
-        assert bench.measured_traffic(workload, b, "dr_stream", sym) is not None, workload
+    import kbgen
+    for workload in ("large", "train"):
+        w = kbgen.WORKLOADS[workload]
+        b = w.batch
+        for phase, rows in (("fwd_stream", w.n_relations), ("dx_stream", w.n_relations),
+                            ("dr_stream", w.n_entities)):
+            lpt, lds = bench.stream_launch(b, rows)
+            sym = bench.stream_kernel_symbol(b, lds=lds, lpt=lpt)
+            assert bench.measured_traffic(workload, b, phase, sym) is not None, (workload, phase)
 
 
 def test_more_than_one_gpu_is_refused():
@@ -121,3 +127,14 @@ def test_stream_launch_mirrors_the_library_rule(bench):
     assert bench.stream_launch(256, 1000, hard=False) == (32, False)
     assert bench.stream_kernel_symbol(256, lds=True, lpt=8) == \
         "_ZN3kbf12_GLOBAL__N_113stream_kernelILi4ELi8ELb1ELb0ELb0ELb1EEEvNS_10StreamArgsE"
+
+
+def test_overlap_backward_rule(bench, monkeypatch):
+    """bench's mirror of the library's rule for the concurrent backward."""
+    monkeypatch.delenv("KBFOLLOW_OVERLAP_BACKWARD", raising=False)
+    assert not bench.overlap_backward((1 << 20) - 1)
+    assert bench.overlap_backward(1 << 20)
+    monkeypatch.setenv("KBFOLLOW_OVERLAP_BACKWARD", "0")
+    assert not bench.overlap_backward(50_000_000)
+    monkeypatch.setenv("KBFOLLOW_OVERLAP_BACKWARD", "1")
+    assert bench.overlap_backward(5000)
