@@ -119,13 +119,14 @@ def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False, l
             f"EEEvNS_10StreamArgsE")
 
 
-def overlap_backward(n_triples):
+def overlap_backward(n_triples, b):
     """Whether the library runs the backward's dR pass concurrently with dX
-    (from 2^20 triples unless KBFOLLOW_OVERLAP_BACKWARD says otherwise)."""
+    (from 2^20 triples at b <= 32 unless KBFOLLOW_OVERLAP_BACKWARD says
+    otherwise)."""
     env = os.environ.get("KBFOLLOW_OVERLAP_BACKWARD")
     if env:
         return env != "0"
-    return n_triples >= (1 << 20)
+    return n_triples >= (1 << 20) and b <= 32
 
 
 def measured_traffic(workload, b, phase, symbol):
@@ -495,7 +496,7 @@ def main():
         # launch durations overlap and are no per-kernel cost, so the
         # roofline is then taken on the forward stream kernel, which runs
         # alone; otherwise on the slowest of the three.
-        candidates = ("fwd_stream",) if overlap_backward(kb.n_triples) else \
+        candidates = ("fwd_stream",) if overlap_backward(kb.n_triples, b) else \
             ("fwd_stream", "dx_stream", "dr_stream")
         dom = max(candidates, key=lambda p: phases[p][0])
         gkb.profile(True, phases=[dom])
@@ -553,7 +554,7 @@ def main():
         roof = {"bound": "hbm", "achieved": round(comp_b / sec / 1e9, 1), "peak": PEAK_HBM_GBPS,
                 "kernel_choice": ("forward stream kernel: dX and dR run concurrently, so their "
                                   "launch durations overlap" if dom == "fwd_stream"
-                                  and overlap_backward(kb.n_triples) else
+                                  and overlap_backward(kb.n_triples, b) else
                                   "the slowest of the three stream kernels"),
                 "unit": "GB/s", "frac": round(comp_b / sec / 1e9 / PEAK_HBM_GBPS, 4),
                 "traffic": traffic,

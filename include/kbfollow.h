@@ -30,7 +30,7 @@
  * NULL = the null stream) and returns; it never synchronises the host and
  * never allocates device memory.  Scratch space comes from the caller's
  * `workspace`, sized with kb_workspace_size().  On KBs of 2^20 triples or
- * more, kb_follow_backward runs its dR pass on a stream the KB owns, forked
+ * more, at b <= 32, kb_follow_backward runs its dR pass on a stream the KB owns, forked
  * from `stream` with an event and joined back into it before returning, so
  * that work enqueued on `stream` afterwards still follows both passes (and
  * a graph captured on `stream` contains both).
@@ -106,7 +106,8 @@ typedef enum {
  *                                       every KB (bitwise the same);
  *   KBFOLLOW_OVERLAP_BACKWARD=0|1       dR concurrent with dX on the KB's
  *                                       own stream (default: from 2^20
- *                                       triples; bitwise the same);
+ *                                       triples at b <= 32; 1 also forces it
+ *                                       on small KBs; bitwise the same);
  *   KBFOLLOW_HOST_THREADS               host threads for the layout sorts
  *                                       (default: the hardware's, at most 16;
  *                                       the same layouts for any count).

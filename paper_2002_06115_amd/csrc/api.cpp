@@ -78,9 +78,10 @@ struct kb_t {
   bool plain_loads = false;  // force plain loads instead of raw buffer loads (testing)
   bool b_in_lds = true;      // stage small B tables in LDS (off: B rows in registers)
   // The backward's dR pass on a stream of the KB's own, concurrent with the
-  // dX pass (large KBs only): fork and join events, and a lock that keeps
-  // one call's record / wait sequence whole when threads share the KB.
-  bool overlap_backward = false;
+  // dX pass: -1 on large KBs at b <= 32, 1 always, 0 never; the stream, fork
+  // and join events, and a lock that keeps one call's record / wait
+  // sequence whole when threads share the KB (side is null when never).
+  int overlap_backward = 0;
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   mutable std::mutex side_mu;
@@ -355,12 +356,16 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     if (kb->n_cu <= 0) kb->n_cu = 1;
     kb->plain_loads = env_int("KBFOLLOW_PLAIN_LOADS", 0) != 0;
     kb->b_in_lds = env_int("KBFOLLOW_B_IN_LDS", 1) != 0;
-    // dR concurrent with dX from 2^20 triples on (measured: large KB step
-    // 2.66 -> 2.56 ms; on small KBs the fork and join cost more than they
-    // save).
-    kb->overlap_backward =
-        env_int("KBFOLLOW_OVERLAP_BACKWARD", n_triples >= (int64_t(1) << 20) ? 1 : 0) != 0;
-    if (kb->overlap_backward) {
+    // dR concurrent with dX from 2^20 triples on, at b <= 32 (measured on the
+    // large KB: steps 3-5 % shorter at b = 8 .. 32, 4 % longer at b = 64, the
+    // same at 128 and 256; on small KBs the fork and join cost more than
+    // they save).
+    {
+      const int forced = env_int("KBFOLLOW_OVERLAP_BACKWARD", -1);
+      kb->overlap_backward = forced >= 0 ? (forced != 0 ? 1 : 0)
+                                         : (n_triples >= (int64_t(1) << 20) ? -1 : 0);
+    }
+    if (kb->overlap_backward != 0) {
       hipError_t e2 = hipStreamCreateWithFlags(&kb->side, hipStreamNonBlocking);
       if (e2 == hipSuccess) e2 = hipEventCreateWithFlags(&kb->ev_fork, hipEventDisableTiming);
       if (e2 == hipSuccess) e2 = hipEventCreateWithFlags(&kb->ev_join, hipEventDisableTiming);
@@ -539,7 +544,8 @@ kb_status backward_impl(const kb_t *kb, int32_t b, const float *X, const float *
     // caller's: the two passes read the same dY, write disjoint arrays and
     // slots, and one's start overlaps the other's tail launches.
     void *dr_ws = static_cast<char *>(workspace) + dr_slots_offset(kb, b);
-    const bool overlap = want_dx && want_dr && kb->overlap_backward;
+    const bool overlap = want_dx && want_dr && kb->side &&
+                         (kb->overlap_backward == 1 || (kb->overlap_backward == -1 && b <= 32));
     std::unique_lock<std::mutex> lock(kb->side_mu, std::defer_lock);
     hipStream_t dr_s = s;
     if (overlap) {

@@ -132,9 +132,10 @@ def test_stream_launch_mirrors_the_library_rule(bench):
 def test_overlap_backward_rule(bench, monkeypatch):
     """bench's mirror of the library's rule for the concurrent backward."""
     monkeypatch.delenv("KBFOLLOW_OVERLAP_BACKWARD", raising=False)
-    assert not bench.overlap_backward((1 << 20) - 1)
-    assert bench.overlap_backward(1 << 20)
+    assert not bench.overlap_backward((1 << 20) - 1, 32)
+    assert bench.overlap_backward(1 << 20, 32)
+    assert not bench.overlap_backward(1 << 20, 64)
     monkeypatch.setenv("KBFOLLOW_OVERLAP_BACKWARD", "0")
-    assert not bench.overlap_backward(50_000_000)
+    assert not bench.overlap_backward(50_000_000, 32)
     monkeypatch.setenv("KBFOLLOW_OVERLAP_BACKWARD", "1")
-    assert bench.overlap_backward(5000)
+    assert bench.overlap_backward(5000, 256)
