@@ -110,3 +110,43 @@ def test_overlap_two_callers_share_the_kb(kbf, monkeypatch):
         for k in (0, 1):
             for name, g, e in zip(("dX", "dR"), outs[k], alone[k]):
                 assert torch.equal(bits(g), bits(e)), f"rep {rep} caller {k} {name}"
+
+
+def test_overlap_two_host_threads(kbf, monkeypatch):
+    """Two host threads, each with its own stream, call the concurrent
+    backward on one KB at the same time: the per-KB lock keeps each call's
+    fork / join sequence whole, and every result equals the one computed
+    alone."""
+    import threading
+    import torch
+    w, kb = workload(11)
+    gkb = make(kbf, w, kb, True, monkeypatch)
+    w2 = kbgen.METAQA.scaled(20_000, 150_000, batch=32, tag=12)
+    ins = [(to_em(kbgen.make_x(v)), to_em(kbgen.make_r(v)), to_em(kbgen.make_dy(v)))
+           for v in (w, w2)]
+    alone = [gkb.follow_backward(*i) for i in ins]
+    torch.cuda.synchronize()
+    results, errors = [[], []], []
+
+    def worker(k):
+        try:
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.default_stream())
+            with torch.cuda.stream(s):
+                for _ in range(20):
+                    results[k].append(gkb.follow_backward(*ins[k]))
+            s.synchronize()
+        except Exception as e:  # reported below, in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in (0, 1)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for k in (0, 1):
+        assert len(results[k]) == 20
+        for i, (dX, dR) in enumerate(results[k]):
+            assert torch.equal(bits(dX), bits(alone[k][0])), f"thread {k} call {i} dX"
+            assert torch.equal(bits(dR), bits(alone[k][1])), f"thread {k} call {i} dR"
