@@ -618,8 +618,11 @@ def main():
                    "x": w.x_kind, "r": w.r_kind, "dy": w.dy_kind, "parallelism": "single GPU",
                    "op": "follow" if args.residual is None else f"follow + {args.residual} * X"},
         "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
+        "concurrent_backward": overlap_backward(kb.n_triples, b),
         "phases_note": ("HIP-event times per phase from a separate loop of the same steps; the "
-                        "timed steps bracket only the roofline's kernel with events"),
+                        "timed steps bracket only the roofline's kernel with events; with "
+                        "concurrent_backward the dx_* and dr_* phases run at the same time, so "
+                        "their times overlap"),
         "kb_create_s": round(create_s, 2),
         "timing": detail,
         "roofline": roof,
