@@ -539,10 +539,11 @@ kb_status backward_impl(const kb_t *kb, int32_t b, const float *X, const float *
     if ((st = check_device(kb)) != KB_OK) return st;
     g_last_error.clear();
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // dR's slots follow dX's in the workspace.  On a large KB the dR pass
-    // runs on the KB's own stream, forked from and joined back into the
-    // caller's: the two passes read the same dY, write disjoint arrays and
-    // slots, and one's start overlaps the other's tail launches.
+    // dR's slots follow dX's in the workspace.  On a large KB at b <= 32
+    // (or when forced) the dR pass runs on the KB's own stream, forked from
+    // and joined back into the caller's: the two passes read the same dY,
+    // write disjoint arrays and slots, and one's start overlaps the other's
+    // tail launches.
     void *dr_ws = static_cast<char *>(workspace) + dr_slots_offset(kb, b);
     const bool overlap = want_dx && want_dr && kb->side &&
                          (kb->overlap_backward == 1 || (kb->overlap_backward == -1 && b <= 32));
