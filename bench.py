@@ -6,16 +6,25 @@ workload is the large KB: 10 M entities, 600 relations, 50 M distinct triples
 with Zipf subject/object/relation marginals, b = 32, 1 %-dense X.
 
 Prints one JSON line with the whole-step throughput (triple-batch products per
-second, N_T * b / step time), a roofline entry for the dominant kernel (HIP
-event time inside the timed region) and the CPU oracle timed on a bounded
-sample of the same workload.
+second, N_T * b / step time), a roofline entry for the dominant kernel (the
+kernel with the largest share of the step's GPU time, its launches timed with
+HIP events inside the timed region), the CPU oracle timed on the same
+workload, and the largest deviation of the GPU's outputs from the oracle's.
+
+Other modes: ``--workload chain3`` (the three-hop chain of the multi-hop
+model, forward + loss + backward per step), ``--grid N`` (the relation sweep
+of the grid scalability experiment), ``--oracle-table`` (the oracle alone,
+per workload and thread count), ``--copy-calibration`` (a plain copy kernel
+for scaling rocprofv3's byte counters).
 """
 from __future__ import annotations
 
 import argparse
+import glob
 import json
 import os
 import platform
+import re
 import sys
 import time
 
@@ -26,16 +35,35 @@ sys.path.insert(0, ROOT)
 
 METRIC = "triple·batch products/sec for kb_follow fwd+bwd; achieved HBM GB/s vs peak"
 PEAK_HBM_GBPS = 8000.0
-DOMINANT_KERNEL_NAMES = {
-    "fwd_stream": "stream_kernel (forward: objects, gathers X and R)",
-    "dx_stream": "stream_kernel (dX: subjects, gathers dY and R)",
-    "dr_stream": "stream_kernel (dR: relations, gathers X and dY)",
-}
+PASSES = ("fwd", "dx", "dr")  # forward (rows = objects), dX (subjects), dR (relations)
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def host_threads(cap=16):
+    """Host cores this process may use (its affinity mask), at most `cap`."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, cap))
+
+
+# ---------------------------------------------------------------------------
+# byte models
+# ---------------------------------------------------------------------------
 
 _DISTINCT = {}
 
@@ -48,159 +76,136 @@ def distinct_ids(kb):
     return _DISTINCT[key]
 
 
-def pass_bytes(kb, b, phase, whole_pass=False):
-    """Algorithmic bytes of one stream-kernel launch under three models, all
-    with the index stream (8 B per triple), the row offsets and R:
-      gather      every triple's b-wide operand rows come from memory;
-      compulsory  each distinct gathered row once (rows no triple names are
+def pass_bytes(kb, b, p, whole_pass=False):
+    """Algorithmic bytes of one pass's stream-kernel launch (or, with
+    whole_pass, of the whole pass: every output row, as the stream kernel and
+    the empty-row fill write them together), hard KB, under three models;
+    every model has the index stream (8 B per triple), the row boundaries and
+    the B table read once:
+      array_once  each gathered array read once in full (the compulsory
+                  model of the method: X, or dY, once; dY and X once for dR);
+      distinct    each distinct gathered row once (rows no triple names are
                   never read);
-      array_once  each operand array read once in full.
-    The stream kernel writes the output rows that have triples; with
-    whole_pass the rows without triples (written by the zero fill) count
-    too, as for the whole pass."""
+      gather      every triple's b-wide rows come from memory.
+    The stream kernel writes the output rows that have triples."""
     n_t, n_e, n_r = kb.n_triples, kb.n_entities, kb.n_relations
     idx = 8 * n_t
     n_subj, n_obj = distinct_ids(kb)
-    if phase in ("fwd_stream", "dx_stream"):
-        n_a, n_out = (n_subj, n_obj) if phase == "fwd_stream" else (n_obj, n_subj)
+    if p in ("fwd", "dx"):
+        n_a, n_out = (n_subj, n_obj) if p == "fwd" else (n_obj, n_subj)
         out = 4 * b * (n_e if whole_pass else n_out)
-        gather = idx + 4 * (n_e + 1) + 4 * b * n_t + 4 * b * n_r + out    # A gathered per triple
-        comp = idx + 4 * (n_e + 1) + 4 * b * n_a + 4 * b * n_r + out
-        once = idx + 4 * (n_e + 1) + 4 * b * n_e + 4 * b * n_r + out
-    else:
-        gather = idx + 4 * (n_r + 1) + 8 * b * n_t + 4 * b * n_r
-        comp = idx + 4 * (n_r + 1) + 4 * b * (n_subj + n_obj) + 4 * b * n_r
-        once = idx + 4 * (n_r + 1) + 8 * b * n_e + 4 * b * n_r
-    return float(gather), float(comp), float(once)
+        base = idx + 4 * (n_e + 1) + 4 * b * n_r + out
+        return {"array_once": float(base + 4 * b * n_e), "distinct": float(base + 4 * b * n_a),
+                "gather": float(base + 4 * b * n_t)}
+    base = idx + 4 * (n_r + 1) + 4 * b * n_r
+    return {"array_once": float(base + 8 * b * n_e),
+            "distinct": float(base + 4 * b * (n_subj + n_obj)),
+            "gather": float(base + 8 * b * n_t)}
 
 
-def column_tiling(b):
-    """(VEC, LPT): 4 floats per lane when b % 4 == 0 (else 1), lanes per group
-    b / VEC rounded up to a power of two, at most 32."""
-    vec = 4 if b % 4 == 0 else 1
-    lanes, lpt = -(-b // vec), 1
-    while lpt < lanes and lpt < 32:
-        lpt *= 2
-    return vec, lpt
+# ---------------------------------------------------------------------------
+# kernel names, fingerprints and the committed rocprofv3 counters
+# ---------------------------------------------------------------------------
+
+def mangled_name(short):
+    """Itanium-mangled symbol of a kernel named as profilers print it
+    ("stream_kernel<4, 8, true, false, false, true>")."""
+    m = re.fullmatch(r"(\w+)<([^>]*)>", short.strip())
+    if not m:
+        return None
+    name, args = m.group(1), [a.strip() for a in m.group(2).split(",")]
+    enc = "".join(f"Lb{1 if a == 'true' else 0}E" if a in ("true", "false") else f"Li{a}E"
+                  for a in args)
+    params = {"stream_kernel": "NS_10StreamArgsE", "tail_kernel": "NS_8TailArgsE",
+              "combine_kernel": "PK15HIP_vector_typeIiLj4EElPdliPflPKff"}.get(name)
+    if params is None:
+        return None
+    return f"_ZN3kbf12_GLOBAL__N_1{len(name)}{name}I{enc}EEv{params}"
 
 
-MAX_LDS_B = 80 * 1024     # B slice staged in LDS with two workgroups per CU
-MAX_LDS_BIG = 160 * 1024  # with one workgroup per CU (hard KB only)
-
-
-def stream_launch(b, b_rows, hard=True):
-    """(LPT, lds) of the stream kernel a pass launches for batch b when its B
-    table has b_rows rows (R for forward and dX, X for dR): B in LDS when its
-    column slice fits (hard KB: rows cut into 32-column slices where that
-    makes it fit).  The library also needs the LDS variant to keep at least as
-    many waves on a CU as the register variant, which holds for the hard-KB,
-    non-residual variants at b >= 32."""
-    vec, lpt = column_tiling(b)
-    if b_rows * vec * lpt * 4 <= MAX_LDS_B:
-        return lpt, True
-    if not hard:
-        return lpt, False
-    narrow = 8 if vec == 4 and lpt > 8 else lpt
-    if b_rows * vec * narrow * 4 <= MAX_LDS_BIG:
-        return narrow, True
-    return lpt, False
-
-
-def stream_kernel_symbol(b, weighted=False, residual=False, plain_loads=False, lds=False,
-                         lpt=None):
-    """Mangled name of the stream-kernel instance a pass launches for batch b:
-    lane layout from column_tiling (or lpt lanes per group), raw-buffer loads
-    unless a table reaches 4 GB, B staged in LDS (lds) or held in registers."""
-    vec, lpt0 = column_tiling(b)
-    lpt = lpt or lpt0
-    flag = lambda v: 1 if v else 0
-    return (f"_ZN3kbf12_GLOBAL__N_113stream_kernelILi{vec}ELi{lpt}ELb{flag(not plain_loads)}"
-            f"ELb{flag(weighted)}ELb{flag(residual)}ELb{flag(lds and not plain_loads)}"
-            f"EEEvNS_10StreamArgsE")
-
-
-def overlap_backward(n_triples, b):
-    """Whether the library runs the backward's dR pass concurrently with dX
-    (from 2^20 triples at b <= 32 unless KBFOLLOW_OVERLAP_BACKWARD says
-    otherwise)."""
-    env = os.environ.get("KBFOLLOW_OVERLAP_BACKWARD")
-    if env:
-        return env != "0"
-    return n_triples >= (1 << 20) and b <= 32
-
-
-def measured_traffic(workload, b, phase, symbol):
-    """DRAM bytes of one launch from the committed rocprofv3 counters, if they
-    were taken on the device code of the kernel that is built now (same
-    per-kernel assembly digest; a profile lists the kernel of each pass under
-    "kernels", else one kernel for all)."""
-    import glob
-    fp_path = os.path.join(ROOT, "paper_2002_06115_amd", "_lib", "kernels.fingerprint")
+def kernel_digest(short):
+    """sha256 of the built kernel's gfx950 assembly (as the build records it)."""
+    path = os.path.join(ROOT, "paper_2002_06115_amd", "_lib", "kernels.fingerprint")
     try:
-        digest = json.load(open(fp_path)).get(symbol)
+        return json.load(open(path)).get(mangled_name(short) or "")
     except (OSError, ValueError):
         return None
+
+
+def measured_traffic(workload, b, short, phases):
+    """Bytes per launch of kernel `short` from the committed rocprofv3
+    counters (FETCH_SIZE and WRITE_SIZE, copy-calibrated) when they were taken
+    on the device code built now (same assembly digest) for this workload and
+    batch: the mean over the launches of `phases`.  Returns (bytes, source)
+    or (None, reason)."""
+    digest = kernel_digest(short)
     if not digest:
-        return None
-    for path in glob.glob(os.path.join(ROOT, "profiles", "*.json")):
+        return None, "no fingerprint for the built kernel"
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.json"))):
         try:
             prof = json.load(open(path))
         except (OSError, ValueError):
             continue
-        k = prof.get("kernels", {}).get(phase, prof)
-        if prof.get("workload") == workload and prof.get("batch") == b \
-                and k.get("symbol") == symbol and k.get("kernel_sha") == digest \
-                and phase in prof.get("per_launch", {}):
-            return float(prof["per_launch"][phase]["bytes"])
-    return None
+        if prof.get("workload") != workload or prof.get("batch") != b:
+            continue
+        per = prof.get("per_launch", {})
+        kern = prof.get("kernels", {})
+        vals = []
+        for ph in phases:
+            k = kern.get(ph, {})
+            if k.get("kernel") == short and k.get("kernel_sha") == digest and ph in per:
+                vals.append(float(per[ph]["bytes"]))
+        if vals and len(vals) == len(phases):
+            return float(np.mean(vals)), \
+                f"{os.path.relpath(path, ROOT)} (fingerprint-matched; FETCH_SIZE and WRITE_SIZE " \
+                f"per dispatch, copy-calibrated)"
+    return None, "no committed counters for the device code built now"
 
 
-def cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads, runs=3):
-    """The oracle on the host cores: forward and backward (dX + dR) timed
-    separately, median of `runs` runs on `threads` threads over `cols` batch
-    columns, plus one thread on one column."""
+# ---------------------------------------------------------------------------
+# the oracle on the host
+# ---------------------------------------------------------------------------
+
+def oracle_pass_times(kb, X_bm, R_bm, dY_bm, threads, runs):
+    """Median seconds of the oracle's forward, dX and dR (each alone) over
+    `runs` runs on `threads` threads, all batch columns, plus the outputs of
+    the last run."""
     import oracle
-    s, r, o = kb.subj, kb.rel, kb.obj
-    n_e, n_r = kb.n_entities, kb.n_relations
-    Xs, Rs, dYs = X_bm[:cols], R_bm[:cols], dY_bm[:cols]
-    oracle.follow(s[:1000], r[:1000], o[:1000], n_e, n_r, Xs[:1], Rs[:1])  # load + warm
-
-    def timed(c, nthreads):
+    args = (kb.subj, kb.rel, kb.obj, kb.n_entities, kb.n_relations)
+    t = {"fwd": [], "dx": [], "dr": []}
+    out = {}
+    for _ in range(runs):
         t0 = time.perf_counter()
-        oracle.follow(s, r, o, n_e, n_r, Xs[:c], Rs[:c], nthreads=nthreads)
+        out["Y"] = oracle.follow(*args, X_bm, R_bm, nthreads=threads)
         t1 = time.perf_counter()
-        oracle.follow_backward(s, r, o, n_e, n_r, Xs[:c], Rs[:c], dYs[:c], nthreads=nthreads)
-        return t1 - t0, time.perf_counter() - t1
-
-    multi = sorted((timed(cols, threads) for _ in range(runs)), key=sum)[runs // 2]
-    fwd_s, bwd_s = multi
-    dt = fwd_s + bwd_s
-    one = timed(1, 1)
-    return {
-        "value": kb.n_triples * cols / dt,
-        "unit": "triple·batch/s",
-        "cores": int(min(threads, cols)),
-        "kind": "oracle",
-        "sample": (f"same KB, {cols} of {X_bm.shape[0]} batch columns, forward {fwd_s:.2f} s + "
-                   f"backward (dX + dR) {bwd_s:.2f} s, median of {runs} runs on "
-                   f"{min(threads, cols)} threads of {os.cpu_count()} ({cpu_model()})"),
-        "fwd_s": round(fwd_s, 3),
-        "bwd_s": round(bwd_s, 3),
-        "single_thread_value": kb.n_triples / sum(one),
-        "single_thread_sample": (f"1 batch column on 1 thread, forward {one[0]:.2f} s + "
-                                 f"backward {one[1]:.2f} s"),
-    }
+        out["dX"], _ = oracle.follow_backward(*args, X_bm, R_bm, dY_bm, want_dr=False,
+                                              nthreads=threads)
+        t2 = time.perf_counter()
+        _, out["dR"] = oracle.follow_backward(*args, X_bm, R_bm, dY_bm, want_dx=False,
+                                              nthreads=threads)
+        t3 = time.perf_counter()
+        t["fwd"].append(t1 - t0)
+        t["dx"].append(t2 - t1)
+        t["dr"].append(t3 - t2)
+    med = {k: float(np.median(v)) for k, v in t.items()}
+    return med, out
 
 
-def cpu_model():
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
-    except OSError:
-        pass
-    return platform.processor() or platform.machine()
+def tolerance_ratio(got, want, atol=1e-7, rtol=1e-5, block=1 << 24):
+    """max over elements of |got - want| / (atol + rtol |want|), in blocks."""
+    g, w = got.reshape(-1), want.reshape(-1)
+    worst = 0.0
+    for i in range(0, g.size, block):
+        gi = g[i:i + block].astype(np.float64)
+        wi = w[i:i + block].astype(np.float64)
+        if gi.size:
+            worst = max(worst, float((np.abs(gi - wi) / (atol + rtol * np.abs(wi))).max()))
+    return worst
 
+
+# ---------------------------------------------------------------------------
+# GPU timing helpers
+# ---------------------------------------------------------------------------
 
 def percentiles(v):
     q = np.percentile(np.asarray(v, dtype=np.float64), [10, 50, 90])
@@ -251,110 +256,397 @@ def graph_step_ms(torch, step, iters):
     return round(t0.elapsed_time(t1) / iters, 4)
 
 
-def probe_lib():
-    """The measurement library (libkbprobe.so), or None when it is not built."""
-    import ctypes
-    from paper_2002_06115_amd import build as kbuild
-    if not os.path.exists(kbuild.PROBE_LIB):
-        return None
-    lib = ctypes.CDLL(kbuild.PROBE_LIB)
-    P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
-    F = ctypes.POINTER(ctypes.c_float)
-    lib.kbp_gather_time.argtypes = [P, I64, I32, P, I32, P, I32, P, F]
-    lib.kbp_stream_read_time.argtypes = [P, I64, I32, P, I32, P, F]
-    lib.kbp_stream_copy_time.argtypes = [P, P, I64, I32, I32, P, F]
-    lib.kbp_stream_write_time.argtypes = [P, I64, I32, I32, P, F]
-    return lib
-
-
-def stream_rates(torch, lib, reps=10):
-    """Device streaming rates on a 2 GiB buffer (best over a few grid sizes):
-    sequential read GB/s, copy GB/s (bytes read + written) and non-temporal
-    zero-fill GB/s."""
-    import ctypes
+def device_stream_rates(torch, reps=10):
+    """The device's streaming rates on a 2 GiB buffer, with torch's own
+    elementwise kernels: a copy (GB/s read + written) and a fill (GB/s
+    written)."""
     n = (2 << 30) // 4
     src = torch.ones(n, device="cuda")
     dst = torch.empty_like(src)
-    read, copy, write = [], [], []
-    for blocks in (1024, 4096, 16384):
-        scratch = torch.empty(blocks * 256, device="cuda")
-        ms = ctypes.c_float()
-        if lib.kbp_stream_read_time(src.data_ptr(), n // 4, blocks, scratch.data_ptr(), reps,
-                                    None, ctypes.byref(ms)) != 0:
-            raise SystemExit("kbp_stream_read_time failed")
-        read.append(4 * n / (ms.value * 1e-3) / 1e9)
-        if lib.kbp_stream_copy_time(src.data_ptr(), dst.data_ptr(), n // 4, blocks, reps, None,
-                                    ctypes.byref(ms)) != 0:
-            raise SystemExit("kbp_stream_copy_time failed")
-        copy.append(2 * 4 * n / (ms.value * 1e-3) / 1e9)
-        if lib.kbp_stream_write_time(dst.data_ptr(), n // 4, blocks, reps, None,
-                                     ctypes.byref(ms)) != 0:
-            raise SystemExit("kbp_stream_write_time failed")
-        write.append(4 * n / (ms.value * 1e-3) / 1e9)
-    del src, dst, scratch
-    return round(max(read), 1), round(max(copy), 1), round(max(write), 1)
+    torch.mul(src, 1.0, out=dst)
+    dst.fill_(0.0)
+    t = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    t[0].record()
+    for _ in range(reps):
+        torch.mul(src, 1.0, out=dst)
+    t[1].record()
+    for _ in range(reps):
+        dst.fill_(0.0)
+    t[2].record()
+    torch.cuda.synchronize()
+    copy = 2 * 4 * n * reps / (t[0].elapsed_time(t[1]) * 1e-3) / 1e9
+    fill = 4 * n * reps / (t[1].elapsed_time(t[2]) * 1e-3) / 1e9
+    del src, dst
+    return round(copy, 1), round(fill, 1)
 
 
-def gather_probe(args, torch, kbgen, kbf):
-    """The memory system's own rate for each pass's row reads: a pure gather
-    (libkbprobe.so, no products, no second operand, no output rows) of the
-    index stream a pass reads per triple, beside the pass's stream-kernel
-    time, plus uniformly random indices for reference."""
-    import ctypes
-    lib = probe_lib()
-    if lib is None:
-        raise SystemExit("libkbprobe.so is not built (run __graft_entry__.build())")
+def phase_groups(kernels, phases_ms):
+    """Phases grouped by the kernel they launch: {kernel: [phases]} over the
+    phases that ran (with launches)."""
+    groups = {}
+    for ph, name in kernels.items():
+        if name and phases_ms.get(ph, (0.0, 0))[1] > 0:
+            groups.setdefault(name, []).append(ph)
+    return groups
+
+
+def dominant_kernel(kernels, phases):
+    """(kernel, its phases, {kernel: ms per step}, why): the kernel with the
+    largest share of the step's GPU time (sum of its launches' durations).
+    Where that is not a stream kernel (small KBs, whose combine and empty-row
+    launches take longer than their stream kernels) the stream kernel with the
+    largest share is taken, since only the stream kernels have a byte model."""
+    groups = phase_groups(kernels, phases)
+    share = {k: sum(phases[p][0] for p in ps) for k, ps in groups.items()}
+    top = max(share, key=share.get)
+    why = "largest share of the step's GPU time (sum of launch durations)"
+    if not all(p.endswith("_stream") for p in groups[top]):
+        streams = [k for k, ps in groups.items() if all(p.endswith("_stream") for p in ps)]
+        top2 = max(streams, key=share.get)
+        why = (f"the stream kernel with the largest share of the step's GPU time ({top}, a "
+               f"combine / empty-row kernel, has more)")
+        top = top2
+    return top, groups[top], share, why
+
+
+def roofline_entry(kb, w, b, kernels, phases, timed, ms_step, residual):
+    """The roofline of the dominant kernel: the one with the largest share of
+    the step's GPU time (sum of its launches' durations).  achieved =
+    algorithmic bytes of its launches (array-once model: each gathered array
+    read once, every output row the kernel writes) / their duration."""
+    dom, dom_phases, share, choice = dominant_kernel(kernels, phases)
+    total = sum(share.values()) or 1.0
+    ms_sum = sum(timed[p][0] for p in dom_phases)
+    launches = sum(timed[p][1] for p in dom_phases)
+    ms_avg = ms_sum / max(1, launches)
+    models = [pass_bytes(kb, b, p.split("_")[0]) for p in dom_phases]
+    per_launch = {m: float(np.mean([x[m] for x in models])) for m in models[0]}
+    sec = ms_avg * 1e-3
+    ach = per_launch["array_once"] / sec / 1e9
+    traffic, source = measured_traffic(w.name, b, dom, dom_phases)
+    roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM_GBPS, 4), "traffic": traffic,
+            "traffic_source": source,
+            "kernel": dom, "phases": dom_phases,
+            "kernel_choice": choice,
+            "gpu_time_share": round(share[dom] / total, 4),
+            "kernel_ms": round(ms_avg, 4), "launches_timed": int(launches),
+            "bytes_model": "array-once: 8 B of ids per triple, the row boundaries, each gathered "
+                           "array read once in full, the B table once, every output row the "
+                           "kernel writes once (hard KB)",
+            "algorithmic_bytes": per_launch["array_once"],
+            "distinct_rows_bytes": per_launch["distinct"],
+            "distinct_rows_frac": round(per_launch["distinct"] / sec / 1e9 / PEAK_HBM_GBPS, 4),
+            "gather_model_bytes": per_launch["gather"],
+            "gather_model_GBps": round(per_launch["gather"] / sec / 1e9, 1)}
+    if traffic:
+        roof["fabric_traffic_GBps"] = round(traffic / sec / 1e9, 1)
+        roof["fabric_traffic_frac_upper_bound"] = round(traffic / sec / 1e9 / PEAK_HBM_GBPS, 4)
+        roof["fabric_traffic_note"] = ("L2-to-fabric bytes: HBM plus Infinity Cache hits, and "
+                                       "every re-read; an upper bound on HBM bytes, not useful "
+                                       "bandwidth")
+        roof["traffic_over_algorithmic"] = round(traffic / per_launch["array_once"], 3)
+    # Every pass (stream kernel + its combine and empty-row launches) and the
+    # whole step against the array-once bytes of whole passes.
+    per_pass = {}
+    for p in PASSES:
+        ms = sum(phases[f"{p}_{s}"][0] for s in ("stream", "tail", "combine"))
+        by = pass_bytes(kb, b, p, whole_pass=True)["array_once"]
+        per_pass[p] = {"ms": round(ms, 4), "bytes": by,
+                       "frac": round(by / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4) if ms else None}
+    step_bytes = sum(pass_bytes(kb, b, p, whole_pass=True)["array_once"] for p in PASSES)
+    roof["per_pass"] = per_pass
+    roof["step"] = {"ms": round(ms_step, 4), "array_once_bytes": step_bytes,
+                    "array_once_frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+                                             4),
+                    "target_frac": 0.6,
+                    "note": "the fwd + dX + dR step against the array-once bytes of the three "
+                            "passes; the >= 0.6 of HBM peak target on the 10 M-entity KB is "
+                            "judged on this figure"}
+    if residual is not None:
+        roof["note"] = "byte models are those of the plain follow; the residual hop also reads " \
+                       "one row of X (dY) per written row"
+    return roof
+
+
+# ---------------------------------------------------------------------------
+# modes
+# ---------------------------------------------------------------------------
+
+def seeds_of(w, extra=None):
+    import kbgen
+    d = {"root": kbgen.ROOT_SEED, "workload_index": w.index, "scale_tag": w.scale_tag,
+         "streams": {"triples": kbgen.ST_TRIPLES, "x": kbgen.ST_X, "r": kbgen.ST_R,
+                     "dy": kbgen.ST_DY, "target": kbgen.ST_TARGET, "perm": kbgen.ST_PERM},
+         "recipe": "numpy PCG64(SeedSequence([root, workload_index, stream, scale_tag, sub"
+                   "(, example)]))"}
+    if extra:
+        d.update(extra)
+    return d
+
+
+def follow_bench(args, torch, kbgen, kbf):
     w = kbgen.WORKLOADS[args.workload]
+    t0 = time.perf_counter()
     kb = kbgen.make_kb(w)
+    X_bm, R_bm, dY_bm = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
+    stats = kb.stats()
+    log(f"[bench] generated {w.label} in {time.perf_counter() - t0:.1f} s; stats {stats}")
+
     torch.cuda.set_device(0)
-    em = lambda a: torch.from_numpy(a).cuda().t().contiguous()
-    X, R, dY = em(kbgen.make_x(w)), em(kbgen.make_r(w)), em(kbgen.make_dy(w))
-    b, chunk = w.batch, 256
+    t0 = time.perf_counter()
     gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
-    Y, dX, dR = torch.empty_like(X), torch.empty_like(X), torch.empty_like(R)
-    gkb.follow(X, R, out=Y)
-    gkb.follow_backward(X, R, dY, dX=dX, dR=dR)
+    torch.cuda.synchronize()
+    create_s = time.perf_counter() - t0
+    log(f"[bench] kb_create {create_s:.1f} s, info {gkb.info()}")
+    em = lambda a: torch.from_numpy(a).cuda().t().contiguous()
+    X, R, dY = em(X_bm), em(R_bm), em(dY_bm)
+    b = w.batch
+    Y = torch.empty_like(X)
+    dX = torch.empty_like(X)
+    dR = torch.empty_like(R)
+    stream = torch.cuda.current_stream()
+    kernels = gkb.phase_kernels(b, residual=args.residual is not None)
+
+    def step():
+        gkb.follow(X, R, out=Y, stream=stream, residual=args.residual)
+        gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream, residual=args.residual)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} done")
+
+    # Events around a phase cost a few microseconds of GPU time each, so the
+    # per-phase breakdown comes from a loop of its own, and the timed steps
+    # bracket only the launches of the dominant kernel.
+    phases, dom_phases = {}, None
+    if not args.no_profile:
+        gkb.profile(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        raw = gkb.profile_read()
+        gkb.profile(False)
+        phases = {k: (v[0] / args.steps, v[1] / args.steps) for k, v in raw.items()}
+        dom_phases = dominant_kernel(kernels, phases)[1]
+        gkb.profile(True, phases=dom_phases)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    timed = gkb.profile_read() if dom_phases else None
+    gkb.profile(False)
+    ms_step = ms_total / args.steps
+    value = kb.n_triples * b / (ms_step * 1e-3)
+    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.3e} triple*batch/s")
+
+    detail = None
+    iters = args.detail_iters
+    if iters < 0:
+        iters = {"tiny": 1000, "metaqa": 200}.get(w.name, 50)
+    if iters > 0:
+        fwd = lambda: gkb.follow(X, R, out=Y, stream=stream, residual=args.residual)
+        bwd = lambda: gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream,
+                                          residual=args.residual)
+        detail = {"warm": timing_detail(torch, fwd, bwd, stream, iters)}
+        flush = torch.empty((1 << 30) // 4, device="cuda")
+        detail["cold"] = timing_detail(torch, fwd, bwd, stream, iters, flush=flush)
+        del flush
+        detail["graph_ms_per_step"] = graph_step_ms(
+            torch, lambda: (gkb.follow(X, R, out=Y, residual=args.residual),
+                            gkb.follow_backward(X, R, dY, dX=dX, dR=dR, residual=args.residual)),
+            iters)
+        detail["copy_GBps"], detail["fill_GBps"] = device_stream_rates(torch)
+        log(f"[bench] detail {json.dumps(detail)}")
+
+    roof = roofline_entry(kb, w, b, kernels, phases, timed, ms_step, args.residual) \
+        if dom_phases else None
+    if roof and detail:
+        roof["device_copy_GBps"] = detail["copy_GBps"]
+        roof["achieved_frac_of_copy"] = round(roof["achieved"] / detail["copy_GBps"], 4)
+
+    cpu, parity = None, None
+    if not args.no_cpu_baseline:
+        # The oracle on all b columns, median of 3 runs, on the host's cores;
+        # its outputs also check every element of this run's GPU outputs.
+        step()
+        torch.cuda.synchronize()
+        threads = host_threads(args.cpu_threads) if args.cpu_threads > 0 else host_threads()
+        threads = min(threads, b)
+        log(f"[bench] timing the CPU oracle on {b} batch columns, {threads} threads")
+        gY, gdX, gdR = (t.t().contiguous().cpu().numpy() for t in (Y, dX, dR))
+        if args.residual is None:
+            med, out = oracle_pass_times(kb, X_bm, R_bm, dY_bm, threads, runs=3)
+            dt = med["fwd"] + med["dx"] + med["dr"]
+            cpu = {"value": kb.n_triples * b / dt, "unit": "triple·batch/s", "cores": threads,
+                   "kind": "oracle",
+                   "sample": (f"the whole workload: all {b} batch columns, forward "
+                              f"{med['fwd']:.2f} s + dX {med['dx']:.2f} s + dR {med['dr']:.2f} s, "
+                              f"median of 3 runs on {threads} threads ({cpu_model()}, "
+                              f"{os.cpu_count()} logical CPUs)"),
+                   "fwd_s": round(med["fwd"], 3), "dx_s": round(med["dx"], 3),
+                   "dr_s": round(med["dr"], 3)}
+            parity = {"compared": "every element of Y, dX and dR against the oracle "
+                                  "(atol 1e-7, rtol 1e-5)",
+                      "max_tol_ratio": {k: round(tolerance_ratio(g, out[k]), 6)
+                                        for k, g in (("Y", gY), ("dX", gdX), ("dR", gdR))}}
+            log(f"[bench] oracle {cpu['value']:.3e} triple*batch/s; parity {parity}")
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "triple·batch/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 in/out, f64 accumulate",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n_entities": w.n_entities, "n_relations": w.n_relations,
+                   "n_triples": kb.n_triples, "batch": b,
+                   "laws": {"subj": w.subj_law, "obj": w.obj_law, "rel": w.rel_law},
+                   "x": w.x_kind, "r": w.r_kind, "dy": w.dy_kind, "parallelism": "single GPU",
+                   "op": "follow" if args.residual is None else f"follow + {args.residual} * X"},
+        "seeds": seeds_of(w),
+        "kb_sha256": kb.sha256(),
+        "kb_stats": stats,
+        "kernels": {k: v for k, v in kernels.items() if v},
+        "phases_ms_per_step": {k: round(v[0], 4) for k, v in phases.items()},
+        "concurrent_backward": _overlap(kb.n_triples, b),
+        "phases_note": ("HIP-event times per phase from a separate loop of the same steps; the "
+                        "timed steps bracket only the dominant kernel's launches with events; "
+                        "with concurrent_backward the dx_* and dr_* phases run at the same "
+                        "time, so their times overlap"),
+        "kb_create_s": round(create_s, 2),
+        "timing": detail,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
+    gkb.close()
+
+
+def _overlap(n_triples, b):
+    """Whether the library runs the backward's dR pass concurrently with dX
+    (from 2^20 triples at b <= 32 unless KBFOLLOW_OVERLAP_BACKWARD says
+    otherwise)."""
+    env = os.environ.get("KBFOLLOW_OVERLAP_BACKWARD")
+    if env:
+        return env != "0"
+    return n_triples >= (1 << 20) and b <= 32
+
+
+def chain_bench(args, torch, kbgen, kbf):
+    """The three-hop chain of the multi-hop model (Sec. 3.2) as one training
+    step on the GPU: r^t = softmax(rho^t), x^t = L1-normalised follow(x^{t-1},
+    r^t) for t = 1..3, softmax cross-entropy against the target set, and the
+    full backward to x^0 and rho^1..rho^3 -- follow kernels and chain glue
+    kernels only."""
+    from paper_2002_06115_amd import chain
+    w = kbgen.CHAIN3
+    kb = kbgen.make_kb(w)
+    x0, rho, tgt = kbgen.make_chain_inputs(w, kb)
+    hops, b = len(rho), w.batch
+    torch.cuda.set_device(0)
+    gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
+    em = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda().t().contiguous()
+    x0e, tgte = em(x0), em(tgt)
+    rhoe = [em(r) for r in rho]
+    kernels = gkb.phase_kernels(b)
+
+    def step():
+        xs, rs, sums = [x0e], [], []
+        for t in range(hops):
+            r = chain.softmax(rhoe[t])
+            rs.append(r)
+            x, s = chain.l1_normalize(gkb.follow(xs[-1], r))
+            sums.append(s)
+            xs.append(x)
+        loss, _, dx = chain.softmax_xent(xs[-1], tgte)
+        drho = [None] * hops
+        for t in range(hops, 0, -1):
+            du = chain.l1_normalize_backward(xs[t], sums[t - 1], dx)
+            dx, dr = gkb.follow_backward(xs[t - 1], rs[t - 1], du)
+            drho[t - 1] = chain.softmax_backward(rs[t - 1], dr)
+        return loss, dx, drho
+
+    for _ in range(args.warmup):
+        step()
     torch.cuda.synchronize()
     gkb.profile(True)
     for _ in range(args.steps):
-        gkb.follow(X, R, out=Y)
-        gkb.follow_backward(X, R, dY, dX=dX, dR=dR)
-    ph = gkb.profile_read()
+        step()
+    torch.cuda.synchronize()
+    raw = gkb.profile_read()
     gkb.profile(False)
-    passes = {k: round(ph[k][0] / max(1, ph[k][1]), 4) for k in ("fwd_stream", "dx_stream",
-                                                                  "dr_stream")}
-    stream_read, stream_copy, stream_write = stream_rates(torch, lib)
-    log(f"[probe] 2 GiB sequential read {stream_read} GB/s, copy {stream_copy} GB/s, "
-        f"zero fill {stream_write} GB/s")
-    lay = {which: kbf.layout_host(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations, which)
-           for which in (0, 1, 2)}
-    rng = np.random.default_rng(np.random.SeedSequence([20020615, 99]))
-    streams = [
-        ("forward: subjects in object order, rows of X", lay[0][1], X),
-        ("dX: objects in subject order, rows of dY", lay[1][1], dY),
-        ("dR: objects in relation order, rows of dY", lay[2][1], dY),
-        ("dR: subjects in relation order, rows of X", lay[2][2], X),
-        ("uniform random entity ids, rows of X",
-         rng.integers(0, w.n_entities, kb.n_triples).astype(np.int32), X),
-    ]
-    rows = []
-    for name, ids, table in streams:
-        idx = torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).cuda()
-        n = idx.numel()
-        out = torch.empty(((n + chunk - 1) // chunk) * b, device="cuda")
-        ms = ctypes.c_float()
-        rc = lib.kbp_gather_time(idx.data_ptr(), n, chunk, table.data_ptr(), b, out.data_ptr(),
-                                 max(1, args.steps), ctypes.c_void_p(None), ctypes.byref(ms))
-        if rc != 0:
-            raise SystemExit(f"kbp_gather_time failed ({rc})")
-        rows.append({"stream": name, "rows": n, "ms": round(ms.value, 4),
-                     "gathered_GBps": round(n * 4 * b / (ms.value * 1e-3) / 1e9, 1)})
-        log(f"[probe] {name}: {ms.value:.4f} ms")
-        del idx, out
-    print(json.dumps({"metric": "pure-gather time of each pass's per-triple row reads",
-                      "config": {"workload": w.name, "batch": b, "chunk": chunk},
-                      "stream_kernel_ms": passes, "sequential_read_GBps": stream_read,
-                      "copy_GBps": stream_copy, "probe": rows}), flush=True)
+    phases = {k: (v[0] / args.steps, v[1] / args.steps) for k, v in raw.items()}
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        res = step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    value = hops * kb.n_triples * b / (ms_step * 1e-3)
+    loss_g, dx_g, drho_g = float(res[0]), res[1].t().contiguous().cpu().numpy(), \
+        [d.t().contiguous().cpu().numpy() for d in res[2]]
+    log(f"[chain3] {ms_step:.4f} ms/step, {value:.3e} triple*batch/s")
+
+    cpu, parity = None, None
+    if not args.no_cpu_baseline:
+        from oracle import chain as ochain
+        arrays = (kb.subj, kb.rel, kb.obj)
+        runs = 20
+        ts = []
+        for _ in range(runs):
+            t0 = time.perf_counter()
+            loss_o, dx_o, drho_o = ochain.chain_grad(arrays, w.n_entities, w.n_relations, x0,
+                                                     rho, tgt)
+            ts.append(time.perf_counter() - t0)
+        dt = float(np.median(ts))
+        cpu = {"value": hops * kb.n_triples * b / dt, "unit": "triple·batch/s", "cores": 1,
+               "kind": "oracle",
+               "sample": (f"the whole step (3 hops forward in double, loss, backward), median of "
+                          f"{runs} runs, {dt * 1e3:.1f} ms, one thread ({cpu_model()})")}
+        parity = {"compared": "loss, every element of dx0 and of drho1..3 against the chain "
+                              "oracle (atol 1e-7, rtol 1e-5)",
+                  "loss_abs_diff": abs(loss_g - loss_o),
+                  "max_tol_ratio": {"dx0": round(tolerance_ratio(dx_g, dx_o), 6),
+                                    **{f"drho{t + 1}": round(tolerance_ratio(drho_g[t], drho_o[t]),
+                                                             6) for t in range(hops)}}}
+    groups = phase_groups(kernels, phases)
+    share = {k: sum(phases[p][0] for p in ps) for k, ps in groups.items()}
+    out = {
+        "metric": METRIC, "value": value, "unit": "triple·batch/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32 in/out, f64 accumulate", "data": "synthetic",
+        "config": {"workload": w.name, "n_entities": w.n_entities,
+                   "n_relations": w.n_relations, "n_triples": kb.n_triples, "batch": b,
+                   "hops": hops, "parallelism": "single GPU",
+                   "op": "3 x (softmax(rho), follow, L1 normalise), softmax cross-entropy, "
+                         "backward to x0 and rho1..3",
+                   "value_definition": "hops * N_T * b / step time"},
+        "seeds": seeds_of(w), "kb_sha256": kb.sha256(), "kb_stats": kb.stats(),
+        "phases_ms_per_step": {k: round(v[0], 4) for k, v in phases.items()},
+        "kernel_ms_per_step": {k: round(v, 4) for k, v in share.items()},
+        "roofline": {"bound": "latency", "achieved": None, "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": None, "traffic": None,
+                     "note": "a 1 k-entity KB: each launch moves a few MB at most; the step is "
+                             "bound by launch and kernel latency, not by HBM bandwidth"},
+        "cpu_baseline": cpu, "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
     gkb.close()
 
 
@@ -393,16 +685,61 @@ def grid_sweep(args, torch, kbgen, kbf):
                       "sweep": rows}), flush=True)
 
 
+def oracle_table(args, kbgen):
+    """The oracle alone on each workload's full inputs: forward, dX and dR
+    timed separately (median of `runs`), at each thread count; one JSON line
+    per (workload, threads), printed as it is measured."""
+    names = args.oracle_workloads.split(",")
+    for name in names:
+        w = kbgen.WORKLOADS[name]
+        t0 = time.perf_counter()
+        kb = kbgen.make_kb(w)
+        if name == "chain3":
+            x0, rho, tgt = kbgen.make_chain_inputs(w, kb)
+        else:
+            X_bm, R_bm, dY_bm = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
+        log(f"[oracle] generated {w.label} in {time.perf_counter() - t0:.1f} s")
+        counts = sorted({int(t) for t in args.oracle_threads.split(",")})
+        for threads in counts:
+            if name == "chain3":
+                if threads != 1:
+                    continue  # the chain oracle (double precision) runs on one thread
+                from oracle import chain as ochain
+                runs = args.oracle_runs or 20
+                ts = []
+                for _ in range(runs):
+                    t1 = time.perf_counter()
+                    ochain.chain_grad((kb.subj, kb.rel, kb.obj), w.n_entities, w.n_relations, x0,
+                                      rho, tgt)
+                    ts.append(time.perf_counter() - t1)
+                dt = float(np.median(ts))
+                rec = {"workload": name, "threads": 1, "runs": runs,
+                       "step_s": round(dt, 6),
+                       "triple_batch_per_s": 3 * kb.n_triples * w.batch / dt}
+            else:
+                th = min(threads, w.batch)
+                runs = args.oracle_runs or (3 if w.n_triples > 10_000_000 else 20)
+                med, _ = oracle_pass_times(kb, X_bm, R_bm, dY_bm, th, runs)
+                dt = med["fwd"] + med["dx"] + med["dr"]
+                rec = {"workload": name, "threads": th, "runs": runs,
+                       "fwd_s": round(med["fwd"], 6), "dx_s": round(med["dx"], 6),
+                       "dr_s": round(med["dr"], 6), "fwd_bwd_s": round(dt, 6),
+                       "triple_batch_per_s": kb.n_triples * w.batch / dt}
+            rec["cpu"] = cpu_model()
+            rec["logical_cpus"] = os.cpu_count()
+            print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="large",
-                    help="tiny | metaqa | large | train (kbgen workload names)")
-    ap.add_argument("--cpu-cols", type=int, default=0,
-                    help="batch columns the oracle times (0 = all b)")
-    ap.add_argument("--cpu-threads", type=int, default=16)
+                    help="tiny | metaqa | chain3 | large | train (kbgen workload names)")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="host threads for the oracle (0: the cores this process may use, "
+                         "at most 16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the HIP-event phase timing")
     ap.add_argument("--residual", type=float, default=None, metavar="GAMMA",
@@ -416,9 +753,12 @@ def main():
     ap.add_argument("--detail-iters", type=int, default=-1,
                     help="iterations of the per-pass timing with percentiles, warm and cold "
                          "cache (-1: 50 for the large KBs, 200 for metaqa, 1000 for tiny; 0: skip)")
-    ap.add_argument("--gather-probe", action="store_true",
-                    help="instead: time a pure gather of each pass's per-triple row reads "
-                         "(the memory system's rate for that access pattern) beside the passes")
+    ap.add_argument("--oracle-table", action="store_true",
+                    help="instead: time the oracle alone (no GPU) per workload and thread count")
+    ap.add_argument("--oracle-workloads", default="tiny,metaqa,chain3,large,train")
+    ap.add_argument("--oracle-threads", default="1,16")
+    ap.add_argument("--oracle-runs", type=int, default=0,
+                    help="runs per median (0: 3 for the KBs over 10 M triples, else 20)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (to scale rocprofv3 "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -428,8 +768,12 @@ def main():
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
-    import torch
     import kbgen
+    if args.oracle_table:
+        oracle_table(args, kbgen)
+        return
+
+    import torch
     import paper_2002_06115_amd as kbf
 
     if args.copy_calibration:
@@ -442,193 +786,13 @@ def main():
         print(json.dumps({"copy_calibration": {"bytes_read": 4 * n, "bytes_written": 4 * n,
                                                "launches": 5}}))
         return
-
     if args.grid:
         grid_sweep(args, torch, kbgen, kbf)
         return
-    if args.gather_probe:
-        gather_probe(args, torch, kbgen, kbf)
+    if args.workload == "chain3":
+        chain_bench(args, torch, kbgen, kbf)
         return
-
-    w = kbgen.WORKLOADS[args.workload]
-    if w.name == "chain3":
-        raise SystemExit("chain3 is a parity case, not a bench workload")
-    t0 = time.perf_counter()
-    kb = kbgen.make_kb(w)
-    X_bm, R_bm, dY_bm = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
-    log(f"[bench] generated {w.label} in {time.perf_counter() - t0:.1f} s; stats {kb.stats()}")
-
-    torch.cuda.set_device(0)
-    t0 = time.perf_counter()
-    gkb = kbf.KB(kb.subj, kb.rel, kb.obj, w.n_entities, w.n_relations)
-    torch.cuda.synchronize()
-    create_s = time.perf_counter() - t0
-    log(f"[bench] kb_create {create_s:.1f} s, info {gkb.info()}")
-    em = lambda a: torch.from_numpy(a).cuda().t().contiguous()
-    X, R, dY = em(X_bm), em(R_bm), em(dY_bm)
-    b = w.batch
-    Y = torch.empty_like(X)
-    dX = torch.empty_like(X)
-    dR = torch.empty_like(R)
-    stream = torch.cuda.current_stream()
-
-    def step():
-        gkb.follow(X, R, out=Y, stream=stream, residual=args.residual)
-        gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream, residual=args.residual)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    log(f"[bench] warmup {args.warmup} done")
-
-    # Events around a phase cost a few microseconds of GPU time each, so the
-    # per-phase breakdown comes from a loop of its own, and the timed steps
-    # bracket only the dominant stream kernel (the roofline's kernel).
-    phases, dom = {}, None
-    if not args.no_profile:
-        gkb.profile(True)
-        for _ in range(args.steps):
-            step()
-        torch.cuda.synchronize()
-        phases = gkb.profile_read()
-        gkb.profile(False)
-        # With the backward's dX and dR passes running concurrently their
-        # launch durations overlap and are no per-kernel cost, so the
-        # roofline is then taken on the forward stream kernel, which runs
-        # alone; otherwise on the slowest of the three.
-        candidates = ("fwd_stream",) if overlap_backward(kb.n_triples, b) else \
-            ("fwd_stream", "dx_stream", "dr_stream")
-        dom = max(candidates, key=lambda p: phases[p][0])
-        gkb.profile(True, phases=[dom])
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms_total = start.elapsed_time(stop)
-    dom_timed = gkb.profile_read()[dom] if dom else None
-    gkb.profile(False)
-    ms_step = ms_total / args.steps
-    value = kb.n_triples * b / (ms_step * 1e-3)
-    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.3e} triple*batch/s")
-
-    detail = None
-    iters = args.detail_iters
-    if iters < 0:
-        iters = {"tiny": 1000, "metaqa": 200}.get(w.name, 50)
-    if iters > 0:
-        fwd = lambda: gkb.follow(X, R, out=Y, stream=stream, residual=args.residual)
-        bwd = lambda: gkb.follow_backward(X, R, dY, dX=dX, dR=dR, stream=stream,
-                                          residual=args.residual)
-        detail = {"warm": timing_detail(torch, fwd, bwd, stream, iters)}
-        flush = torch.empty((1 << 30) // 4, device="cuda")
-        detail["cold"] = timing_detail(torch, fwd, bwd, stream, iters, flush=flush)
-        del flush
-        detail["graph_ms_per_step"] = graph_step_ms(
-            torch, lambda: (gkb.follow(X, R, out=Y, residual=args.residual),
-                            gkb.follow_backward(X, R, dY, dX=dX, dR=dR, residual=args.residual)),
-            iters)
-        lib = probe_lib()
-        if lib is not None:
-            (detail["stream_read_GBps"], detail["copy_GBps"],
-             detail["write_GBps"]) = stream_rates(torch, lib)
-        log(f"[bench] detail {json.dumps(detail)}")
-
-    roof = None
-    if dom:
-        # The dominant kernel's mean launch time within the timed steps.
-        ms_avg = dom_timed[0] / max(1, dom_timed[1])
-        gather_b, comp_b, once_b = pass_bytes(kb, b, dom)
-        sec = ms_avg * 1e-3
-        b_rows = w.n_entities if dom == "dr_stream" else w.n_relations
-        lpt, lds = stream_launch(b, b_rows, hard=args.residual is None)
-        if os.environ.get("KBFOLLOW_B_IN_LDS") == "0":
-            lpt, lds = None, False
-        symbol = stream_kernel_symbol(b, residual=args.residual is not None,
-                                      plain_loads=os.environ.get("KBFOLLOW_PLAIN_LOADS") == "1",
-                                      lds=lds, lpt=lpt)
-        traffic = measured_traffic(w.name, b, dom, symbol)
-        roof = {"bound": "hbm", "achieved": round(comp_b / sec / 1e9, 1), "peak": PEAK_HBM_GBPS,
-                "kernel_choice": ("forward stream kernel: dX and dR run concurrently, so their "
-                                  "launch durations overlap" if dom == "fwd_stream"
-                                  and overlap_backward(kb.n_triples, b) else
-                                  "the slowest of the three stream kernels"),
-                "unit": "GB/s", "frac": round(comp_b / sec / 1e9 / PEAK_HBM_GBPS, 4),
-                "traffic": traffic,
-                "kernel": DOMINANT_KERNEL_NAMES[dom], "kernel_ms": round(ms_avg, 4),
-                "bytes_model": "compulsory: 8 B of ids per triple, row offsets, every distinct "
-                               "gathered row once, R, every output row once",
-                "algorithmic_bytes": comp_b,
-                "gather_model_bytes": gather_b,
-                "gather_model_GBps": round(gather_b / sec / 1e9, 1),
-                "array_once_bytes": once_b,
-                "array_once_GBps": round(once_b / sec / 1e9, 1),
-                "array_once_frac": round(once_b / sec / 1e9 / PEAK_HBM_GBPS, 4)}
-        # The whole step (fwd + dX + dR and their combine and zero-fill
-        # launches) against the three passes' bytes.
-        step_sec = ms_step * 1e-3
-        step = [pass_bytes(kb, b, p, whole_pass=True) for p in ("fwd_stream", "dx_stream", "dr_stream")]
-        step_comp, step_once = sum(x[1] for x in step), sum(x[2] for x in step)
-        roof["step"] = {"ms": round(ms_step, 4),
-                        "compulsory_bytes": step_comp,
-                        "compulsory_frac": round(step_comp / step_sec / 1e9 / PEAK_HBM_GBPS, 4),
-                        "array_once_bytes": step_once,
-                        "array_once_frac": round(step_once / step_sec / 1e9 / PEAK_HBM_GBPS, 4)}
-        if traffic:
-            roof["hbm_measured_GBps"] = round(traffic / sec / 1e9, 1)
-            roof["hbm_measured_frac"] = round(traffic / sec / 1e9 / PEAK_HBM_GBPS, 4)
-        if detail and "stream_read_GBps" in detail:
-            # The device's own streaming rates (libkbprobe.so, 2 GiB buffer):
-            # a sequential read, and a copy (bytes read + written).
-            rd, cp = detail["stream_read_GBps"], detail["copy_GBps"]
-            roof["stream_read_GBps"] = rd
-            roof["copy_GBps"] = cp
-            roof["achieved_frac_of_copy"] = round(comp_b / sec / 1e9 / cp, 4)
-            if traffic:
-                roof["hbm_measured_frac_of_stream_read"] = round(traffic / sec / 1e9 / rd, 4)
-                roof["hbm_measured_frac_of_copy"] = round(traffic / sec / 1e9 / cp, 4)
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        cols = b if args.cpu_cols <= 0 else max(1, min(args.cpu_cols, b))
-        threads = max(1, min(cols, args.cpu_threads, os.cpu_count() or 1))
-        log(f"[bench] timing the CPU oracle on {cols} batch columns, {threads} threads")
-        cpu = cpu_baseline(kb, X_bm, R_bm, dY_bm, cols, threads)
-        log(f"[bench] oracle {cpu['value']:.3e} triple*batch/s")
-
-    out = {
-        "metric": METRIC,
-        "value": value,
-        "unit": "triple·batch/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32 in/out, f64 accumulate",
-        "data": "synthetic",
-        "config": {"workload": w.name, "n_entities": w.n_entities, "n_relations": w.n_relations,
-                   "n_triples": kb.n_triples, "batch": b,
-                   "laws": {"subj": w.subj_law, "obj": w.obj_law, "rel": w.rel_law},
-                   "x": w.x_kind, "r": w.r_kind, "dy": w.dy_kind, "parallelism": "single GPU",
-                   "op": "follow" if args.residual is None else f"follow + {args.residual} * X"},
-        "phases_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in phases.items()},
-        "concurrent_backward": overlap_backward(kb.n_triples, b),
-        "phases_note": ("HIP-event times per phase from a separate loop of the same steps; the "
-                        "timed steps bracket only the roofline's kernel with events; with "
-                        "concurrent_backward the dx_* and dr_* phases run at the same time, so "
-                        "their times overlap"),
-        "kb_create_s": round(create_s, 2),
-        "timing": detail,
-        "roofline": roof,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(out), flush=True)
+    follow_bench(args, torch, kbgen, kbf)
 
 
 if __name__ == "__main__":

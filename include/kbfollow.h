@@ -291,6 +291,17 @@ kb_status kb_profile_select(kb_t *kb, uint32_t phase_mask);
  * then clear the record. */
 kb_status kb_profile_read(kb_t *kb, double *ms, int64_t *launches);
 
+/* The kernel a phase launches for this KB at batch size b, as profilers
+ * print it (e.g. "stream_kernel<4, 8, true, false, false, true>"), written
+ * NUL-terminated into name[len] (truncated if longer); "" when the phase
+ * launches nothing.  residual != 0 describes kb_follow_residual and
+ * kb_follow_backward_residual instead of kb_follow and kb_follow_backward.
+ * Uses the runtime's occupancy calculator on the KB's device (which must be
+ * current) but enqueues nothing.  KB_EINVAL for a NULL kb or name, len = 0,
+ * b < 1 or a phase outside [0, KB_PH_COUNT). */
+kb_status kb_phase_kernel(const kb_t *kb, int32_t b, int32_t phase, int32_t residual, char *name,
+                          size_t len);
+
 #ifdef __cplusplus
 }
 #endif

@@ -90,6 +90,8 @@ def _load_library():
     lib.kb_profile_select.restype = ctypes.c_int
     lib.kb_profile_read.argtypes = [p, p, p]
     lib.kb_profile_read.restype = ctypes.c_int
+    lib.kb_phase_kernel.argtypes = [p, i32, i32, i32, ctypes.c_char_p, sz]
+    lib.kb_phase_kernel.restype = ctypes.c_int
     lib.kb_checked_violations.argtypes = [ctypes.POINTER(ctypes.c_uint64), i32]
     lib.kb_checked_violations.restype = ctypes.c_int
     return lib
@@ -105,10 +107,20 @@ def _check(status, what):
 
 
 def _host_ids(a, n):
-    a = np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+    """A contiguous int32 copy (or view) of an id array; ids that do not fit
+    int32 are rejected here rather than wrapped into a different, in-range id."""
+    a = np.asarray(a)
     if a.shape != (n,):
         raise ValueError("subj, rel and obj must be 1-D arrays of equal length")
-    return a
+    if a.size == 0:
+        return np.empty(0, np.int32)
+    if a.dtype != np.int32:
+        if not np.issubdtype(a.dtype, np.integer):
+            raise TypeError(f"ids must be integers, got {a.dtype}")
+        if int(a.min()) < np.iinfo(np.int32).min or int(a.max()) > np.iinfo(np.int32).max:
+            raise ValueError("ids must fit int32 (the library takes ids below 2^30)")
+        a = a.astype(np.int32)
+    return np.ascontiguousarray(a)
 
 
 def _np_ptr(a):
@@ -307,6 +319,17 @@ class KB:
         for p in phases:
             mask |= 1 << PHASES.index(p)
         _check(_lib.kb_profile_select(self._handle, mask if on else 0), "kb_profile_select")
+
+    def phase_kernels(self, b, residual=False):
+        """{phase: the kernel it launches at batch size b, as profilers print
+        it ("" when the phase launches nothing)}."""
+        out = {}
+        buf = ctypes.create_string_buffer(256)
+        for i, p in enumerate(PHASES):
+            _check(_lib.kb_phase_kernel(self._handle, int(b), i, 1 if residual else 0, buf,
+                                        len(buf)), "kb_phase_kernel")
+            out[p] = buf.value.decode()
+        return out
 
     def profile_read(self):
         """{phase: (total ms, launches)} since the last read."""

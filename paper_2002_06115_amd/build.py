@@ -79,23 +79,6 @@ def build_checked(verbose: bool = False) -> str:
                  build_dir=os.path.join(BUILD_DIR, "checked"))
 
 
-PROBE_LIB = os.path.join(OUT_DIR, "libkbprobe.so")
-
-
-def build_probe(verbose: bool = False) -> str:
-    """Compile the gather-rate probe (a measurement helper used by bench.py,
-    not part of the follow library) into its own shared library."""
-    os.makedirs(OUT_DIR, exist_ok=True)
-    tmp = PROBE_LIB + ".tmp"
-    cmd = [hipcc(), "-x", "hip", *DEVICE_FLAGS, *COMMON_FLAGS, "-shared",
-           os.path.join(CSRC, "gather_probe.hip"), "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.check_call(cmd)
-    os.replace(tmp, PROBE_LIB)
-    return PROBE_LIB
-
-
 def fingerprint(defines, path, bdir, csrc=CSRC) -> dict:
     """Per-kernel sha256 of the gfx950 assembly of kernels.hip, written as JSON
     {mangled kernel name: digest}: identifies the device code that rocprofv3
@@ -148,6 +131,5 @@ def build_chain(verbose: bool = False) -> str:
 
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
-    print(build_probe(verbose="-v" in sys.argv))
     print(build_chain(verbose="-v" in sys.argv))
     print(build_checked(verbose="-v" in sys.argv))

@@ -4,6 +4,8 @@
 
 #include <algorithm>
 #include <climits>
+#include <cstdint>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <exception>
@@ -624,6 +626,46 @@ kb_status kb_checked_violations(uint64_t *count, int32_t reset) {
   if (e != hipSuccess) return hip_fail(e, "reading the violation counter");
   *count = c;
   return KB_OK;
+}
+
+kb_status kb_phase_kernel(const kb_t *kb, int32_t b, int32_t phase, int32_t residual, char *name,
+                          size_t len) {
+  if (!kb || !name || len == 0) return fail(KB_EINVAL, "kb and name must be non-NULL");
+  if (b < 1) return fail(KB_EINVAL, "b must be >= 1");
+  if (phase < 0 || phase >= KB_PH_COUNT) return fail(KB_EINVAL, "no such phase");
+  try {
+    kb_status st = check_device(kb);
+    if (st != KB_OK) return st;
+    const int pass = phase / 3, step = phase % 3;  // pass: fwd, dX, dR; step: stream, tail, combine
+    const DevLayout &D = kb->L[pass == 0 ? BY_OBJ : pass == 1 ? BY_SUBJ : BY_REL];
+    const bool res = residual != 0 && pass != 2;  // the dR pass has no residual term
+    // Placeholder device addresses: the choice depends only on sizes, on
+    // which arrays are present and on whether the added rows come from A.
+    float *const A = reinterpret_cast<float *>(uintptr_t(256));
+    std::string out;
+    if (step == 0) {
+      const int64_t B_rows = pass == 2 ? kb->n_entities : kb->n_relations;
+      StreamArgs a{D.entries, D.weights, D.n,   D.chunk,    A,         kb->n_entities, A,
+                   B_rows,    b,         A,     D.rows,     nullptr,   D.n_slots,      res ? 1 : 0,
+                   1.0f,      res ? A : nullptr};
+      StreamOptions o;
+      o.plain_loads = kb->plain_loads;
+      o.b_in_lds = kb->b_in_lds;
+      o.n_cu = kb->n_cu;
+      out = describe_stream(a, o);
+    } else if (step == 1) {
+      const int64_t n0 = D.level_begin.size() > 1 ? D.level_begin[1] - D.level_begin[0] : 0;
+      TailArgs t{D.ctasks, n0, nullptr, D.n_slots, D.empty, D.n_empty_pieces, b, A, D.rows,
+                 res ? A : nullptr, 1.0f, 0};
+      out = describe_tail(t);
+    } else if (D.level_begin.size() > 2) {
+      out = describe_combine(b);
+    }
+    std::snprintf(name, len, "%s", out.c_str());
+    return KB_OK;
+  } catch (...) {
+    return fail(KB_EINVAL, "unexpected host error");
+  }
 }
 
 kb_status kb_profile_select(kb_t *kb, uint32_t phase_mask) {

@@ -5,6 +5,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <string>
 
 namespace kbf {
 
@@ -71,6 +72,10 @@ struct StreamOptions {
   int n_cu = 1;  // compute units of the device, for the LDS variant's grid
 };
 hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s);
+// The kernel launch_stream would launch for `a`, as profilers print it
+// ("stream_kernel<4, 8, true, false, false, true>"); "" when nothing would be
+// launched.  Likewise for launch_tail and launch_combine.
+std::string describe_stream(const StreamArgs &a, const StreamOptions &o);
 
 // Sums workspace slots in order (one combine level).  A final row write adds
 // gamma * res[row] when res is not null (residual hop, accumulating follow;
@@ -98,6 +103,8 @@ struct TailArgs {
   int64_t combine_blocks;
 };
 hipError_t launch_tail(const TailArgs &a, hipStream_t s);
+std::string describe_tail(const TailArgs &a);
+std::string describe_combine(int32_t b);
 
 // Bounds violations counted by a checked build (KBFOLLOW_CHECKED) on the
 // current device since the last reset; hipErrorNotSupported otherwise.

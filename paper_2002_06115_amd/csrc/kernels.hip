@@ -9,7 +9,7 @@
 //
 //     forward : rows = objects,   A = X  (a = subject),  B = R  (b_id = relation)
 //     dX      : rows = subjects,  A = dY (a = object),   B = R  (b_id = relation)
-//     dR      : rows = relations, A = X  (a = subject),  B = dY (b_id = object)
+//     dR      : rows = relations, A = dY (a = object),   B = X  (b_id = subject)
 //
 // Activations are entity-major and batch-contiguous ([N][b] float32), so each
 // gather is one contiguous b-wide row: a lane group of LPT lanes reads it with
@@ -32,7 +32,9 @@
 #include "plan.h"
 
 #include <climits>
+#include <cstdio>
 #include <map>
+#include <string>
 #include <tuple>
 #include <mutex>
 #include <utility>
@@ -713,8 +715,19 @@ ColumnTiling column_tiling_max(int32_t b, int max_lpt) {
   return t;
 }
 
-hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s) {
-  if (a.n == 0) return hipSuccess;
+namespace {
+
+// The stream-kernel instance, grid and LDS size launch_stream uses for `a`.
+struct StreamChoice {
+  const void *fn = nullptr;
+  dim3 grid;
+  int block = 0;
+  size_t lds_bytes = 0;
+  int vec = 0, lpt = 0;
+  bool buf = false, wt = false, res = false, ldsb = false;
+};
+
+hipError_t choose_stream(const StreamArgs &a, const StreamOptions &o, StreamChoice *c) {
   const ColumnTiling t = column_tiling(a.b);
   if (a.chunk % kChunkQuantum != 0 || a.n % a.chunk != 0) return hipErrorInvalidValue;
   // Raw-buffer offsets are 32-bit: tables of 4 GB or more take plain loads.
@@ -726,10 +739,12 @@ hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_
                    (uint64_t)a.n_slots * (uint64_t)a.b * sizeof(double) <= lim;
   const bool wt = a.weights != nullptr, res = a.residual != 0;
   const int64_t n_chunks = a.n / a.chunk;
-  StreamArgs arg = a;
-  void *params[] = {&arg};
   const void *reg_fn = stream_fn_for(t, buf, false, wt, res);
   if (!reg_fn) return hipErrorInvalidValue;
+  c->buf = buf;
+  c->wt = wt;
+  c->res = res;
+  c->vec = t.vec;
   // B's column slice in LDS when it fits and the LDS variant keeps at least
   // as many waves on a CU as the register variant: where it needs more
   // registers per lane than its workgroup can be given (b = 4 .. 16, the
@@ -758,14 +773,63 @@ hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_
       if (per_cu > 0 && per_cu * blk >= reg_per_cu * kBlock) {
         const int64_t cap = (int64_t)per_cu * (o.n_cu > 0 ? o.n_cu : 1);
         const int64_t cap32 = cap > (int64_t)INT32_MAX ? (int64_t)INT32_MAX : cap;
-        const dim3 grid((unsigned)blocks_for(n_chunks, blk / tl.lpt, (int)cap32),
-                        (unsigned)tl.n_slices);
-        return hipLaunchKernel(fn, grid, dim3(blk), params, lds_bytes, s);
+        c->fn = fn;
+        c->grid = dim3((unsigned)blocks_for(n_chunks, blk / tl.lpt, (int)cap32),
+                       (unsigned)tl.n_slices);
+        c->block = blk;
+        c->lds_bytes = lds_bytes;
+        c->lpt = tl.lpt;
+        c->ldsb = true;
+        return hipSuccess;
       }
     }
   }
-  const dim3 grid((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
-  return hipLaunchKernel(reg_fn, grid, dim3(kBlock), params, 0, s);
+  c->fn = reg_fn;
+  c->grid = dim3((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
+  c->block = kBlock;
+  c->lds_bytes = 0;
+  c->lpt = t.lpt;
+  c->ldsb = false;
+  return hipSuccess;
+}
+
+const char *tf(bool v) { return v ? "true" : "false"; }
+
+}  // namespace
+
+hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s) {
+  if (a.n == 0) return hipSuccess;
+  StreamChoice c;
+  hipError_t e = choose_stream(a, o, &c);
+  if (e != hipSuccess) return e;
+  StreamArgs arg = a;
+  void *params[] = {&arg};
+  return hipLaunchKernel(c.fn, c.grid, dim3(c.block), params, c.lds_bytes, s);
+}
+
+std::string describe_stream(const StreamArgs &a, const StreamOptions &o) {
+  if (a.n == 0) return "";
+  StreamChoice c;
+  if (choose_stream(a, o, &c) != hipSuccess) return "";
+  char buf[160];
+  std::snprintf(buf, sizeof buf, "stream_kernel<%d, %d, %s, %s, %s, %s>", c.vec, c.lpt,
+                tf(c.buf), tf(c.wt), tf(c.res), tf(c.ldsb));
+  return buf;
+}
+
+std::string describe_tail(const TailArgs &a) {
+  if (a.n_tasks == 0 && a.n_pieces == 0) return "";
+  const ColumnTiling t = column_tiling(a.b);
+  char buf[96];
+  std::snprintf(buf, sizeof buf, "tail_kernel<%d, %d, %s>", t.vec, t.lpt, tf(a.res == nullptr));
+  return buf;
+}
+
+std::string describe_combine(int32_t b) {
+  const ColumnTiling t = column_tiling(b);
+  char buf[96];
+  std::snprintf(buf, sizeof buf, "combine_kernel<%d, %d>", t.vec, t.lpt);
+  return buf;
 }
 
 hipError_t launch_combine(const int4 *tasks, int64_t n_tasks, double *slots, int64_t n_slots,

@@ -1,7 +1,7 @@
 """bench.py's own arithmetic and bookkeeping, on the CPU: the byte models of
 the roofline entry (against counts done by hand on a small KB), the mapping
-from batch width to the stream-kernel instance whose counters are looked up,
-the fingerprint gate on committed traffic figures, and the one-GPU guard."""
+from a kernel's profiler name to its symbol in the build, the fingerprint gate
+on committed traffic figures, and the one-GPU guard."""
 import importlib.util
 import json
 import os
@@ -38,72 +38,98 @@ def test_byte_models_by_hand(bench):
     row = 4 * b  # bytes of one b-wide float row
     ids = 8 * 5
     # forward: A = X rows of subjects, output rows = objects with triples
-    g, c, o = bench.pass_bytes(kb, b, "fwd_stream")
-    assert g == ids + 4 * 7 + 5 * row + 3 * row + 2 * row          # every triple's A row
-    assert c == ids + 4 * 7 + 3 * row + 3 * row + 2 * row          # 3 distinct subjects
-    assert o == ids + 4 * 7 + 6 * row + 3 * row + 2 * row          # all of X
+    m = bench.pass_bytes(kb, b, "fwd")
+    assert m["gather"] == ids + 4 * 7 + 5 * row + 3 * row + 2 * row      # every triple's A row
+    assert m["distinct"] == ids + 4 * 7 + 3 * row + 3 * row + 2 * row    # 3 distinct subjects
+    assert m["array_once"] == ids + 4 * 7 + 6 * row + 3 * row + 2 * row  # all of X
     # dX: A = dY rows of objects, output rows = subjects with triples
-    g, c, o = bench.pass_bytes(kb, b, "dx_stream")
-    assert (g, c, o) == (ids + 28 + 5 * row + 3 * row + 3 * row,
-                         ids + 28 + 2 * row + 3 * row + 3 * row,
-                         ids + 28 + 6 * row + 3 * row + 3 * row)
+    m = bench.pass_bytes(kb, b, "dx")
+    assert (m["gather"], m["distinct"], m["array_once"]) == (
+        ids + 28 + 5 * row + 3 * row + 3 * row, ids + 28 + 2 * row + 3 * row + 3 * row,
+        ids + 28 + 6 * row + 3 * row + 3 * row)
     # dR: two gathered rows per triple; R-sized output
-    g, c, o = bench.pass_bytes(kb, b, "dr_stream")
-    assert (g, c, o) == (ids + 4 * 4 + 10 * row + 3 * row,
-                         ids + 4 * 4 + (3 + 2) * row + 3 * row,
-                         ids + 4 * 4 + 12 * row + 3 * row)
+    m = bench.pass_bytes(kb, b, "dr")
+    assert (m["gather"], m["distinct"], m["array_once"]) == (
+        ids + 4 * 4 + 10 * row + 3 * row, ids + 4 * 4 + (3 + 2) * row + 3 * row,
+        ids + 4 * 4 + 12 * row + 3 * row)
     # whole passes count the rows the zero fill writes too
-    assert bench.pass_bytes(kb, b, "fwd_stream", whole_pass=True)[1] == \
+    assert bench.pass_bytes(kb, b, "fwd", whole_pass=True)["distinct"] == \
         ids + 28 + 3 * row + 3 * row + 6 * row
 
 
-def test_kernel_symbols_exist_in_the_build(bench):
+def test_array_once_bytes_of_the_large_kb(bench):
+    """The figures the roofline is judged by, for the 10 M-entity / 50 M-triple
+    KB at b = 32: 2.365 GB per forward / dX stream-kernel launch (5.04 M
+    output rows with triples), 3.00 GB per whole forward or dX pass, 2.96 GB
+    for dR, 8.96 GB per step."""
+    kb = types.SimpleNamespace(n_triples=50_000_000, n_entities=10_000_000, n_relations=600)
+    bench._DISTINCT[id(kb)] = (5_035_558, 5_036_810)
+    fwd = bench.pass_bytes(kb, 32, "fwd")["array_once"]
+    assert abs(fwd - 2.3648e9) < 1e6
+    step = sum(bench.pass_bytes(kb, 32, p, whole_pass=True)["array_once"]
+               for p in ("fwd", "dx", "dr"))
+    assert abs(step - 8.9602e9) < 1e6
+
+
+def test_mangled_names_match_the_build(bench):
+    """Profiler names map onto the build's kernel symbols (whose assembly
+    digests gate the committed traffic figures)."""
     fp = os.path.join(ROOT, "paper_2002_06115_amd", "_lib", "kernels.fingerprint")
     if not os.path.exists(fp):
         pytest.skip("run __graft_entry__.build() first")
     digests = json.load(open(fp))
-    for b in (1, 4, 5, 32, 128, 256, 300):
-        for weighted in (False, True):
-            for residual in (False, True):
-                for plain, lds in ((False, False), (False, True), (True, False)):
-                    sym = bench.stream_kernel_symbol(b, weighted, residual, plain, lds)
-                    assert sym in digests, (b, weighted, residual, plain, lds, sym)
+    for vec in (1, 4):
+        for lpt in (1, 2, 4, 8, 16, 32):
+            for flags in ("true, false, false, false", "true, false, false, true",
+                          "true, true, false, false", "true, false, true, true",
+                          "false, false, false, false", "false, true, true, false"):
+                name = f"stream_kernel<{vec}, {lpt}, {flags}>"
+                assert bench.mangled_name(name) in digests, name
+            assert bench.mangled_name(f"tail_kernel<{vec}, {lpt}, true>") in digests
+            assert bench.mangled_name(f"combine_kernel<{vec}, {lpt}>") in digests
+    assert bench.mangled_name("stream_kernel<4, 8, true, false, false, true>") == \
+        "_ZN3kbf12_GLOBAL__N_113stream_kernelILi4ELi8ELb1ELb0ELb0ELb1EEEvNS_10StreamArgsE"
 
 
 def test_committed_traffic_is_gated_by_the_fingerprint(bench, tmp_path, monkeypatch):
-    sym = bench.stream_kernel_symbol(32)
+    name = "stream_kernel<4, 8, true, false, false, false>"
+    sym = bench.mangled_name(name)
     (tmp_path / "paper_2002_06115_amd" / "_lib").mkdir(parents=True)
     (tmp_path / "profiles").mkdir()
-    prof = {"workload": "large", "batch": 32, "symbol": sym, "kernel_sha": "abc",
+    prof = {"workload": "large", "batch": 32,
+            "kernels": {"dr_stream": {"kernel": name, "kernel_sha": "abc"}},
             "per_launch": {"dr_stream": {"bytes": 123.0}}}
     (tmp_path / "profiles" / "p.json").write_text(json.dumps(prof))
     fp = tmp_path / "paper_2002_06115_amd" / "_lib" / "kernels.fingerprint"
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     fp.write_text(json.dumps({sym: "abc"}))
-    assert bench.measured_traffic("large", 32, "dr_stream", sym) == 123.0
-    assert bench.measured_traffic("large", 32, "fwd_stream", sym) is None
-    assert bench.measured_traffic("train", 32, "dr_stream", sym) is None
+    assert bench.measured_traffic("large", 32, name, ["dr_stream"])[0] == 123.0
+    assert bench.measured_traffic("large", 32, name, ["fwd_stream"])[0] is None
+    assert bench.measured_traffic("large", 32, name, ["dr_stream", "fwd_stream"])[0] is None
+    assert bench.measured_traffic("train", 32, name, ["dr_stream"])[0] is None
     fp.write_text(json.dumps({sym: "changed"}))  # the kernel was rebuilt differently
-    assert bench.measured_traffic("large", 32, "dr_stream", sym) is None
+    assert bench.measured_traffic("large", 32, name, ["dr_stream"])[0] is None
     fp.unlink()
-    assert bench.measured_traffic("large", 32, "dr_stream", sym) is None
+    assert bench.measured_traffic("large", 32, name, ["dr_stream"])[0] is None
 
 
 def test_committed_profiles_match_the_built_kernels(bench):
-    """The traffic figures in profiles/ were taken on the stream kernels built
-    now (otherwise bench.py reports traffic as null)."""
+    """Every kernel a committed profile gives counters for was taken on the
+    device code built now (otherwise bench.py reports its traffic as null):
+    re-take the counters after changing a kernel."""
     fp = os.path.join(ROOT, "paper_2002_06115_amd", "_lib", "kernels.fingerprint")
     if not os.path.exists(fp):
         pytest.skip("run __graft_entry__.build() first")
-    import kbgen
-    for workload in ("large", "train"):
-        w = kbgen.WORKLOADS[workload]
-        b = w.batch
-        for phase, rows in (("fwd_stream", w.n_relations), ("dx_stream", w.n_relations),
-                            ("dr_stream", w.n_entities)):
-            lpt, lds = bench.stream_launch(b, rows)
-            sym = bench.stream_kernel_symbol(b, lds=lds, lpt=lpt)
-            assert bench.measured_traffic(workload, b, phase, sym) is not None, (workload, phase)
+    digests = json.load(open(fp))
+    import glob
+    found = 0
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*.json")):
+        prof = json.load(open(path))
+        for phase, k in prof.get("kernels", {}).items():
+            assert digests.get(bench.mangled_name(k["kernel"])) == k["kernel_sha"], \
+                (os.path.basename(path), phase, k["kernel"])
+            found += 1
+    assert found > 0
 
 
 def test_more_than_one_gpu_is_refused():
@@ -112,30 +138,13 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode != 0 and "one GPU" in r.stderr
 
 
-def test_stream_launch_mirrors_the_library_rule(bench):
-    """bench.stream_launch: (lanes per group, B in LDS) for a pass whose B
-    table has b_rows rows, as the library's launcher chooses it for the hard
-    KB: the default layout when B's slice fits 80 KB, 32-column slices when
-    that makes it fit 160 KB, registers otherwise."""
-    assert bench.stream_launch(32, 600) == (8, True)        # 76.8 KB
-    assert bench.stream_launch(32, 1280) == (8, True)       # 160 KB, one workgroup per CU
-    assert bench.stream_launch(32, 1281) == (8, False)
-    assert bench.stream_launch(128, 160) == (32, True)      # 80 KB at 128 columns
-    assert bench.stream_launch(128, 161) == (8, True)       # cut into 32-column slices
-    assert bench.stream_launch(256, 1000) == (8, True)      # 128 KB per 32-column slice
-    assert bench.stream_launch(256, 10_000_000) == (32, False)
-    assert bench.stream_launch(256, 1000, hard=False) == (32, False)
-    assert bench.stream_kernel_symbol(256, lds=True, lpt=8) == \
-        "_ZN3kbf12_GLOBAL__N_113stream_kernelILi4ELi8ELb1ELb0ELb0ELb1EEEvNS_10StreamArgsE"
-
-
 def test_overlap_backward_rule(bench, monkeypatch):
     """bench's mirror of the library's rule for the concurrent backward."""
     monkeypatch.delenv("KBFOLLOW_OVERLAP_BACKWARD", raising=False)
-    assert not bench.overlap_backward((1 << 20) - 1, 32)
-    assert bench.overlap_backward(1 << 20, 32)
-    assert not bench.overlap_backward(1 << 20, 64)
+    assert not bench._overlap((1 << 20) - 1, 32)
+    assert bench._overlap(1 << 20, 32)
+    assert not bench._overlap(1 << 20, 64)
     monkeypatch.setenv("KBFOLLOW_OVERLAP_BACKWARD", "0")
-    assert not bench.overlap_backward(50_000_000, 32)
+    assert not bench._overlap(50_000_000, 32)
     monkeypatch.setenv("KBFOLLOW_OVERLAP_BACKWARD", "1")
-    assert bench.overlap_backward(5000, 256)
+    assert bench._overlap(5000, 256)

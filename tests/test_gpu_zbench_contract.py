@@ -49,3 +49,33 @@ def test_bench_line_on_the_tiny_workload(monkeypatch, capsys):
     for k in ("value", "unit", "cores", "kind", "sample"):
         assert k in cpu, k
     assert cpu["kind"] == "oracle" and cpu["cores"] >= 1 and cpu["value"] > 0
+    assert d["cpu_baseline"]["sample"].startswith("the whole workload")
+    par = d["parity"]["max_tol_ratio"]
+    assert set(par) == {"Y", "dX", "dR"} and max(par.values()) <= 1.0, par
+    assert d["kb_sha256"] and d["seeds"]["root"] == 20020615 and d["kb_stats"]
+    assert roof["kernel"] in d["kernels"].values()
+    assert roof["step"]["array_once_frac"] > 0
+
+
+def test_bench_line_on_the_chain3_workload(monkeypatch, capsys):
+    """The three-hop chain mode: one line, its value consistent with the step
+    time (three follows per step), and parity with the chain oracle."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", "chain3", "--steps", "5",
+                                      "--warmup", "1"])
+    bench.main()
+    lines = [l for l in capsys.readouterr().out.splitlines() if l.strip()]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    assert d["config"]["workload"] == "chain3" and d["config"]["hops"] == 3
+    n_t, b = d["config"]["n_triples"], d["config"]["batch"]
+    assert abs(d["value"] - 3 * n_t * b / (d["ms_per_step"] * 1e-3)) <= 1e-6 * d["value"]
+    assert d["cpu_baseline"]["kind"] == "oracle" and d["cpu_baseline"]["value"] > 0
+    assert max(d["parity"]["max_tol_ratio"].values()) <= 1.0
+    assert d["parity"]["loss_abs_diff"] <= 1e-7 + 1e-5 * 10

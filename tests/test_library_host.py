@@ -136,3 +136,19 @@ def test_layout_sort_same_for_any_thread_count(kbf, threads, monkeypatch):
     for which, (k1, k2, k3) in specs.items():
         off, ca, cb, perm = kbf.layout_host(s, r, o, n_e, n_r, which)
         assert np.array_equal(perm, np.lexsort((np.arange(n_t), k3, k2, k1))), which
+
+
+def test_host_ids_refuse_ids_that_do_not_fit_int32(kbf):
+    """An int64 id of 2^32 + 5 must not wrap to 5 (a different, in-range KB)."""
+    with pytest.raises(ValueError):
+        kbf._host_ids(np.array([0, (1 << 32) + 5], np.int64), 2)
+    with pytest.raises(ValueError):
+        kbf._host_ids(np.array([-(1 << 31) - 1], np.int64), 1)
+    with pytest.raises(TypeError):
+        kbf._host_ids(np.array([1.0, 2.0]), 2)
+    ids = kbf._host_ids(np.array([3, 1 << 29], np.int64), 2)
+    assert ids.dtype == np.int32 and list(ids) == [3, 1 << 29]
+    assert kbf._host_ids([], 0).dtype == np.int32
+    # Negative ids that fit int32 reach kb_create's own range check (KB_ERANGE).
+    assert list(kbf._host_ids(np.array([-5], np.int64), 1)) == [-5]
+
