@@ -187,6 +187,8 @@ def oracle_pass_times(kb, X_bm, R_bm, dY_bm, threads, runs):
         t["fwd"].append(t1 - t0)
         t["dx"].append(t2 - t1)
         t["dr"].append(t3 - t2)
+        log(f"[oracle] {kb.n_triples} triples, {X_bm.shape[0]} columns, {threads} threads: "
+            f"fwd {t1 - t0:.3f} s, dX {t2 - t1:.3f} s, dR {t3 - t2:.3f} s")
     med = {k: float(np.median(v)) for k, v in t.items()}
     return med, out
 

@@ -281,9 +281,12 @@ kb_status kb_profile_enable(kb_t *kb, int32_t on);
 
 /* Record only the phases whose bit (1u << kb_phase) is set in phase_mask
  * (0 turns recording off); clears the accumulated times like
- * kb_profile_enable.  Each recorded phase adds two events to the stream,
- * and each event costs a few microseconds of GPU time, so a benchmark that
- * times whole steps records only the phases it needs. */
+ * kb_profile_enable.  A STREAM phase (one kernel) is timed by its kernel's
+ * own start and end timestamps (hipExtLaunchKernel), which adds nothing to
+ * the stream; TAIL and COMBINE phases add two events each, and each event
+ * costs a few microseconds of GPU time (and, recorded between the dX pass's
+ * launches, holds back the concurrent dR pass), so a benchmark that times
+ * whole steps records only the phases it needs. */
 kb_status kb_profile_select(kb_t *kb, uint32_t phase_mask);
 
 /* Wait for the recorded events, add their elapsed times into ms[KB_PH_COUNT]

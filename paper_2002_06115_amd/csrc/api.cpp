@@ -182,15 +182,23 @@ struct PhaseScope {
     if (hipEventCreate(&e) != hipSuccess) return nullptr;
     return e;
   }
-  PhaseScope(const kb_t *k, int ph, hipStream_t st) : kb(k), phase(ph), s(st) {
+  // record_events: record start now and stop at the end of the scope;
+  // otherwise the events go to the scope's one kernel launch, which sets
+  // them (see launch_stream), and the scope only files them.
+  bool record_events = true;
+  PhaseScope(const kb_t *k, int ph, hipStream_t st, bool record = true)
+      : kb(k), phase(ph), s(st), record_events(record) {
     if (!((kb->timing.mask >> phase) & 1u)) return;
     start = take(kb->timing);
     stop = take(kb->timing);
-    if (start && stop) (void)hipEventRecord(start, s);
+    if (start && stop && record_events) (void)hipEventRecord(start, s);
   }
+  // The events to hand to the scope's kernel launch (null when not timed).
+  hipEvent_t launch_start() const { return (start && stop && !record_events) ? start : nullptr; }
+  hipEvent_t launch_stop() const { return (start && stop && !record_events) ? stop : nullptr; }
   ~PhaseScope() {
     if (start && stop) {
-      (void)hipEventRecord(stop, s);
+      if (record_events) (void)hipEventRecord(stop, s);
       kb->timing.recs.push_back({phase, start, stop});
       return;
     }
@@ -227,15 +235,17 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
                    void *ws, const float *Z, float gamma, hipStream_t s) {
   double *slots = static_cast<double *>(ws);
   const float *res = Z;
-  {
-    PhaseScope scope(kb, ph_base + 0, s);
+  if (D.n > 0) {
+    // Timed by the kernel's own timestamps: no event packets between this
+    // launch and the next, which would hold back a concurrent pass.
+    PhaseScope scope(kb, ph_base + 0, s, false);
     StreamArgs a{D.entries, D.weights, D.n, D.chunk, A,           A_rows,     B,
                  B_rows,    b,         out,  D.rows,  slots, D.n_slots, Z ? 1 : 0, gamma, Z};
     StreamOptions o;
     o.plain_loads = kb->plain_loads;
     o.b_in_lds = kb->b_in_lds;
     o.n_cu = kb->n_cu;
-    hipError_t e = launch_stream(a, o, s);
+    hipError_t e = launch_stream(a, o, s, scope.launch_start(), scope.launch_stop());
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
   {

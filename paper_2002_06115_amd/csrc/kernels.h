@@ -71,7 +71,11 @@ struct StreamOptions {
   bool b_in_lds = true;
   int n_cu = 1;  // compute units of the device, for the LDS variant's grid
 };
-hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s);
+// With start / stop events the kernel is launched with hipExtLaunchKernel,
+// which sets them to the kernel's own start and end timestamps (no event
+// packets of their own on the stream).
+hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s,
+                         hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 // The kernel launch_stream would launch for `a`, as profilers print it
 // ("stream_kernel<4, 8, true, false, false, true>"); "" when nothing would be
 // launched.  Likewise for launch_tail and launch_combine.

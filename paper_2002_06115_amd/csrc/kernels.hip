@@ -31,6 +31,8 @@
 #include "kernels.h"
 #include "plan.h"
 
+#include <hip/hip_ext.h>
+
 #include <climits>
 #include <cstdio>
 #include <map>
@@ -797,13 +799,16 @@ const char *tf(bool v) { return v ? "true" : "false"; }
 
 }  // namespace
 
-hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s) {
+hipError_t launch_stream(const StreamArgs &a, const StreamOptions &o, hipStream_t s,
+                         hipEvent_t start, hipEvent_t stop) {
   if (a.n == 0) return hipSuccess;
   StreamChoice c;
   hipError_t e = choose_stream(a, o, &c);
   if (e != hipSuccess) return e;
   StreamArgs arg = a;
   void *params[] = {&arg};
+  if (start || stop)
+    return hipExtLaunchKernel(c.fn, c.grid, dim3(c.block), params, c.lds_bytes, s, start, stop, 0);
   return hipLaunchKernel(c.fn, c.grid, dim3(c.block), params, c.lds_bytes, s);
 }
 
