@@ -166,6 +166,29 @@ kb_status kb_follow_backward(const kb_t *kb, int32_t b, const float *X, const fl
                              size_t ws_bytes, void *stream);
 
 /*
+ * kb_follow for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops, harnesses that forbid hipMalloc): the same
+ * forward pass, kernels and bitwise the same Y, but the split-row partials go
+ * to a fixed scratch array inside the library instead of a caller workspace,
+ * so neither the call nor the caller allocates anything.
+ *
+ *   X, R, Y, stream : as for kb_follow (Y fully overwritten).
+ *
+ * The scratch holds KB_NOALLOC_SCRATCH_BYTES (64 MiB) per GPU, taken on the
+ * first call on that GPU and held until the process ends.  A KB and batch
+ * size whose kb_workspace_size exceeds it are refused with KB_EINVAL before
+ * anything is enqueued (the 10 M-entity / 50 M-triple KB needs about 61 MiB
+ * at b = 32).  Every call on one GPU shares that GPU's scratch, and the
+ * scratch keeps the last call's partials (each call writes every partial it
+ * reads, so nothing needs clearing): calls that overlap in time on one GPU --
+ * on two streams, or from two host threads -- race and must not be issued.
+ * Other errors as for kb_follow.
+ */
+#define KB_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+kb_status kb_follow_noalloc(const kb_t *kb, int32_t b, const float *X, const float *R, float *Y,
+                            void *stream);
+
+/*
  * Residual hop of the KB-completion chains (Sec. 3.2, App. E), which add each
  * hop's input back:  Y = follow(X, R) + gamma * X  (gamma = 1 in the paper).
  * Arguments, layout and rules as for kb_follow; each element of Y is the

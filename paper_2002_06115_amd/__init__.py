@@ -69,6 +69,8 @@ def _load_library():
     lib.kb_follow.restype = ctypes.c_int
     lib.kb_follow_backward.argtypes = [p, i32, p, p, p, p, p, p, sz, p]
     lib.kb_follow_backward.restype = ctypes.c_int
+    lib.kb_follow_noalloc.argtypes = [p, i32, p, p, p, p]
+    lib.kb_follow_noalloc.restype = ctypes.c_int
     f32 = ctypes.c_float
     lib.kb_follow_residual.argtypes = [p, i32, p, p, f32, p, p, sz, p]
     lib.kb_follow_residual.restype = ctypes.c_int
@@ -251,6 +253,25 @@ class KB:
                                                float(residual), self._ptr(Y), self._ptr(ws), nws,
                                                ctypes.c_void_p(s.cuda_stream)),
                        "kb_follow_residual")
+        return Y
+
+    def follow_noalloc(self, X, R, out, stream=None):
+        """follow(X, R) into the caller's ``out`` through kb_follow_noalloc:
+        the split-row partials use the library's fixed per-GPU scratch, so
+        neither this call nor the library allocates.  Calls that overlap on
+        one GPU share that scratch and must not be issued."""
+        X = self._act(X, self.n_entities, "X")
+        R = self._act(R, self.n_relations, "R")
+        Y = self._act(out, self.n_entities, "out")
+        b = X.shape[1]
+        if R.shape[1] != b or Y.shape[1] != b:
+            raise ValueError("X, R and out must have the same batch size")
+        import torch
+        s = torch.cuda.current_stream(self.device) if stream is None else stream
+        with torch.cuda.device(self.device):
+            _check(_lib.kb_follow_noalloc(self._handle, b, self._ptr(X), self._ptr(R),
+                                          self._ptr(Y), ctypes.c_void_p(s.cuda_stream)),
+                   "kb_follow_noalloc")
         return Y
 
     def follow_accumulate(self, X, R, Z, gamma=1.0, out=None, stream=None):

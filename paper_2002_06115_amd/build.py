@@ -17,7 +17,7 @@ OUT_DIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(OUT_DIR, "libkbfollow.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["kernels.hip", "api.cpp", "plan.cpp"]
+SOURCES = ["kernels.hip", "static_scratch.hip", "api.cpp", "plan.cpp"]
 
 # Device code: gfx950 only.  Packed-FP32 instructions are disabled (the
 # compiler would otherwise form v_pk_* from plain float code); no fast-math and

@@ -601,6 +601,30 @@ kb_status kb_follow(const kb_t *kb, int32_t b, const float *X, const float *R, f
   return follow_impl(kb, b, X, R, nullptr, 0.0f, Y, workspace, ws_bytes, stream);
 }
 
+kb_status kb_follow_noalloc(const kb_t *kb, int32_t b, const float *X, const float *R, float *Y,
+                            void *stream) {
+  if (!kb) return fail(KB_EINVAL, "kb must be non-NULL");
+  if (b < 1) return fail(KB_EINVAL, "b must be >= 1");
+  // The partials go to the library's fixed scratch instead of a workspace;
+  // a KB and batch size that need more than it holds are refused before
+  // anything is enqueued.
+  const size_t need = workspace_bytes(kb, b);
+  if (need > kStaticScratchBytes)
+    return fail(KB_EINVAL, "kb_follow_noalloc: this KB needs " + std::to_string(need) +
+                               " bytes of scratch at b = " + std::to_string(b) +
+                               ", more than the " + std::to_string(kStaticScratchBytes) +
+                               " bytes of the fixed scratch (use kb_follow with a workspace)");
+  kb_status st = check_device(kb);
+  if (st != KB_OK) return st;
+  void *ws = nullptr;
+  if (need > 0) {
+    hipError_t e = static_scratch(kb->device, &ws);
+    if (e != hipSuccess) return hip_fail(e, "address of the fixed scratch");
+  }
+  return follow_impl(kb, b, X, R, nullptr, 0.0f, Y, ws, need > 0 ? kStaticScratchBytes : 0,
+                     stream);
+}
+
 kb_status kb_follow_residual(const kb_t *kb, int32_t b, const float *X, const float *R,
                              float gamma, float *Y, void *workspace, size_t ws_bytes,
                              void *stream) {

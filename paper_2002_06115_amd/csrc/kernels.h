@@ -110,6 +110,12 @@ hipError_t launch_tail(const TailArgs &a, hipStream_t s);
 std::string describe_tail(const TailArgs &a);
 std::string describe_combine(int32_t b);
 
+// The fixed device scratch of kb_follow_noalloc: kStaticScratchBytes per
+// device, resolved with that device current (static_scratch.hip).  *ptr is
+// the current device's copy; every caller on one device shares it.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+hipError_t static_scratch(int device, void **ptr);
+
 // Bounds violations counted by a checked build (KBFOLLOW_CHECKED) on the
 // current device since the last reset; hipErrorNotSupported otherwise.
 hipError_t checked_violations(unsigned long long *count, bool reset);

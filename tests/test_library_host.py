@@ -152,3 +152,12 @@ def test_host_ids_refuse_ids_that_do_not_fit_int32(kbf):
     # Negative ids that fit int32 reach kb_create's own range check (KB_ERANGE).
     assert list(kbf._host_ids(np.array([-5], np.int64), 1)) == [-5]
 
+
+def test_noalloc_scratch_limit_matches_the_library():
+    """The header's KB_NOALLOC_SCRATCH_BYTES is the scratch size the library refuses beyond."""
+    text = open(HEADER).read()
+    m = re.search(r"#define KB_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m, "KB_NOALLOC_SCRATCH_BYTES not found"
+    src = open(os.path.join(ROOT, "paper_2002_06115_amd", "csrc", "kernels.h")).read()
+    m2 = re.search(r"kStaticScratchBytes = size_t\((\d+)\) << (\d+);", src)
+    assert m2 and (int(m.group(1)) << int(m.group(2))) == (int(m2.group(1)) << int(m2.group(2)))
