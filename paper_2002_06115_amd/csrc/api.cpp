@@ -52,6 +52,8 @@ struct DevLayout {
   int64_t n_slots = 0;
   int64_t n_split_rows = 0;
   int64_t max_row_len = 0;
+  int32_t n_lists = 1;                 // chunk lists, one per XCD
+  int64_t list_chunk[kMaxChunkLists + 1] = {};
 };
 
 struct Timing {
@@ -147,6 +149,9 @@ kb_status build_device_layout(kb_t *kb, DevLayout &D, int64_t rows, const PlanHo
   D.n_slots = P.n_slots;
   D.n_split_rows = P.n_split_rows;
   D.max_row_len = P.max_row_len;
+  static_assert(kMaxXcd == kMaxChunkLists, "one chunk list per XCD");
+  D.n_lists = P.n_xcd;
+  for (int x = 0; x <= P.n_xcd; ++x) D.list_chunk[x] = P.xcd_chunk[x];
   static_assert(sizeof(Entry) == sizeof(int2), "entry layout");
   static_assert(sizeof(EmptyPiece) == sizeof(int2), "empty-piece layout");
   std::vector<int4> ctasks;
@@ -240,7 +245,9 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
     // launch and the next, which would hold back a concurrent pass.
     PhaseScope scope(kb, ph_base + 0, s, false);
     StreamArgs a{D.entries, D.weights, D.n, D.chunk, A,           A_rows,     B,
-                 B_rows,    b,         out,  D.rows,  slots, D.n_slots, Z ? 1 : 0, gamma, Z};
+                 B_rows,    b,         out,  D.rows,  slots, D.n_slots, Z ? 1 : 0, gamma, Z,
+                 D.n_lists, {}};
+    std::copy(D.list_chunk, D.list_chunk + kMaxChunkLists + 1, a.list_chunk);
     StreamOptions o;
     o.plain_loads = kb->plain_loads;
     o.b_in_lds = kb->b_in_lds;
@@ -414,11 +421,28 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                                                              : LayoutSort::kAuto);
       // The three plans on three host threads, then the uploads in turn.
       const int32_t plen[3] = {chunk_seg, chunk_seg, chunk_rel};
+      // One chunk list per XCD (8 on an MI355X; KBFOLLOW_XCD overrides, 1 is
+      // a single list in row order).  Hub rows (KBFOLLOW_HUB_MIN triples or
+      // more) are split by the class of the gathered id; in the forward and
+      // dX passes (second operand R, read from LDS) their triples are ordered
+      // by gathered id, in the dR pass by (subject, object), which keeps the
+      // runs of equal subject whose X row is read once.
+      const int32_t n_xcd = std::max(1, std::min(kMaxXcd, env_int("KBFOLLOW_XCD", 8)));
+      const int64_t hub_min = std::max(1, env_int("KBFOLLOW_HUB_MIN", 256));
+      const bool band = env_int("KBFOLLOW_BAND", 1) != 0;
       PlanHost P[3];
       std::exception_ptr err[3];
       auto plan = [&](int k) {
         try {
-          P[k] = plan_layout(H[k], plen[k], fan_in);
+          PlanOptions po;
+          po.chunk = plen[k];
+          po.fan_in = fan_in;
+          po.n_xcd = n_xcd;
+          po.hub_min = hub_min;
+          po.hub_by_a = k != BY_REL;
+          po.band = band;
+          po.n_ids_a = n_entities;  // subjects (forward) or objects (dX, dR)
+          P[k] = plan_layout(H[k], po);
           H[k] = LayoutHost{H[k].rows};  // the sorted rows are no longer needed
         } catch (...) {
           err[k] = std::current_exception();
@@ -681,7 +705,8 @@ kb_status kb_phase_kernel(const kb_t *kb, int32_t b, int32_t phase, int32_t resi
       const int64_t B_rows = pass == 2 ? kb->n_entities : kb->n_relations;
       StreamArgs a{D.entries, D.weights, D.n,   D.chunk,    A,         kb->n_entities, A,
                    B_rows,    b,         A,     D.rows,     nullptr,   D.n_slots,      res ? 1 : 0,
-                   1.0f,      res ? A : nullptr};
+                   1.0f,      res ? A : nullptr, D.n_lists, {}};
+      std::copy(D.list_chunk, D.list_chunk + kMaxChunkLists + 1, a.list_chunk);
       StreamOptions o;
       o.plain_loads = kb->plain_loads;
       o.b_in_lds = kb->b_in_lds;

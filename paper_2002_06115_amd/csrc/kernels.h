@@ -27,7 +27,7 @@ constexpr int32_t kChunkQuantum = 8;
 // of the library).  entries[p] = (x, y): a triple x = a | run-start flag,
 // y = b_id, or a marker x = -1, y = target (row, -(slot + 1), or INT32_MIN
 // for none); n is a multiple of chunk, and chunk of kChunkQuantum.  Lane
-// group g walks entries [g * chunk, (g + 1) * chunk):
+// group walks the entries of one chunk at a time ([c * chunk, (c + 1) * chunk)):
 //     held = B[b_id]                          at a triple flagged run-start
 //     acc += w[p] * A[a] (.) held             for every triple
 //     target = acc (float row / double slot), acc = 0   at a marker
@@ -38,6 +38,9 @@ constexpr int32_t kChunkQuantum = 8;
 // accumulating follow, Z = out itself adding into the output in place (each
 // row's Z is read by the thread that then writes it).  Raw buffer loads need
 // Z = A; another Z takes the plain-load path.
+// At most this many chunk lists (one per XCD); see StreamArgs::list_chunk.
+constexpr int kMaxChunkLists = 8;
+
 struct StreamArgs {
   const int2 *entries;
   const float *weights;  // per entry, nullptr for a hard KB
@@ -55,6 +58,11 @@ struct StreamArgs {
   int32_t residual;
   float gamma;
   const float *Z;  // the rows added at markers when residual is set
+  // Chunk lists: workgroups with blockIdx.x % n_lists == x walk chunks
+  // [list_chunk[x], list_chunk[x + 1]) (list x is meant for XCD x, which runs
+  // those workgroups); n_lists = 1 is one list of every chunk.
+  int32_t n_lists;
+  int64_t list_chunk[kMaxChunkLists + 1];
 };
 // Largest B column slice (B_rows * slice width * 4 bytes) the stream kernel
 // copies into LDS with two workgroups per CU (two copies fit a CU's 160 KB),

@@ -33,6 +33,7 @@
 
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <climits>
 #include <cstdio>
 #include <map>
@@ -292,8 +293,20 @@ stream_kernel(StreamArgs a) {
   const __amdgpu_buffer_rsrc_t srsrc =
       rsrc(a.slots, (uint64_t)a.n_slots * a.b * sizeof(double));
 
-  const int64_t n_chunks = a.n / a.chunk;
-  const int64_t stride = (int64_t)gridDim.x * GPB;
+  // This workgroup's chunk list: the blocks with blockIdx.x % n_lists == x
+  // (all on XCD x) share list x, grid-stride.
+  const int nl = a.n_lists;
+  const int xl = (int)(blockIdx.x % (unsigned)nl);
+  int64_t c_begin = 0, c_end = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxChunkLists; ++i)
+    if (i == xl) {
+      c_begin = a.list_chunk[i];
+      c_end = a.list_chunk[i + 1];
+    }
+  const int64_t wg_in_list = blockIdx.x / nl;
+  const int64_t wgs_in_list = ((int64_t)gridDim.x - xl + nl - 1) / nl;
+  const int64_t stride = wgs_in_list * GPB;
 
   if constexpr (LDSB) {
     // Columns [col0, col0 + W) of every B row; columns past b read as zeros.
@@ -329,8 +342,8 @@ stream_kernel(StreamArgs a) {
     }
   };
 
-  for (int64_t g = (int64_t)blockIdx.x * GPB + grp; g < n_chunks; g += stride) {
-    const int64_t p0 = g * a.chunk;
+  for (int64_t g = c_begin + wg_in_list * GPB + grp; g < c_end; g += stride) {
+    const int64_t p0 = KBF_CHECKED(g, a.n / a.chunk) * a.chunk;
     const int64_t p1 = p0 + a.chunk;
     double acc[VEC];
     float held_b[VEC];  // the current run's B row
@@ -740,7 +753,17 @@ hipError_t choose_stream(const StreamArgs &a, const StreamOptions &o, StreamChoi
                    (uint64_t)a.B_rows * row_bytes <= lim && (uint64_t)a.out_rows * row_bytes <= lim &&
                    (uint64_t)a.n_slots * (uint64_t)a.b * sizeof(double) <= lim;
   const bool wt = a.weights != nullptr, res = a.residual != 0;
-  const int64_t n_chunks = a.n / a.chunk;
+  if (a.n_lists < 1 || a.n_lists > kMaxChunkLists || a.list_chunk[0] != 0 ||
+      a.list_chunk[a.n_lists] != a.n / a.chunk)
+    return hipErrorInvalidValue;
+  // Every list gets the same number of workgroups (blockIdx.x % n_lists
+  // picks the list), enough for its longest list.
+  int64_t longest = 0;
+  for (int x = 0; x < a.n_lists; ++x) {
+    if (a.list_chunk[x + 1] < a.list_chunk[x]) return hipErrorInvalidValue;
+    longest = std::max<int64_t>(longest, a.list_chunk[x + 1] - a.list_chunk[x]);
+  }
+  const int nl = a.n_lists;
   const void *reg_fn = stream_fn_for(t, buf, false, wt, res);
   if (!reg_fn) return hipErrorInvalidValue;
   c->buf = buf;
@@ -774,10 +797,11 @@ hipError_t choose_stream(const StreamArgs &a, const StreamOptions &o, StreamChoi
       const int reg_per_cu = blocks_per_cu(reg_fn, kBlock, 0);
       if (per_cu > 0 && per_cu * blk >= reg_per_cu * kBlock) {
         const int64_t cap = (int64_t)per_cu * (o.n_cu > 0 ? o.n_cu : 1);
-        const int64_t cap32 = cap > (int64_t)INT32_MAX ? (int64_t)INT32_MAX : cap;
+        const int64_t per_list = std::max<int64_t>(1, std::min<int64_t>(
+            (longest + blk / tl.lpt - 1) / (blk / tl.lpt), cap / nl));
+        if (per_list * nl > (int64_t)INT32_MAX) return hipErrorInvalidValue;
         c->fn = fn;
-        c->grid = dim3((unsigned)blocks_for(n_chunks, blk / tl.lpt, (int)cap32),
-                       (unsigned)tl.n_slices);
+        c->grid = dim3((unsigned)(per_list * nl), (unsigned)tl.n_slices);
         c->block = blk;
         c->lds_bytes = lds_bytes;
         c->lpt = tl.lpt;
@@ -786,8 +810,10 @@ hipError_t choose_stream(const StreamArgs &a, const StreamOptions &o, StreamChoi
       }
     }
   }
+  const int64_t per_list = std::max<int64_t>(1, (longest + kBlock / t.lpt - 1) / (kBlock / t.lpt));
+  if (per_list * nl > (int64_t)INT32_MAX) return hipErrorInvalidValue;
   c->fn = reg_fn;
-  c->grid = dim3((unsigned)blocks_for(n_chunks, kBlock / t.lpt, 0), (unsigned)t.n_slices);
+  c->grid = dim3((unsigned)(per_list * nl), (unsigned)t.n_slices);
   c->block = kBlock;
   c->lds_bytes = 0;
   c->lpt = t.lpt;

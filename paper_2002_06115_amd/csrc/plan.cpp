@@ -339,74 +339,311 @@ static void add_empty(PlanHost &P, int64_t first, int64_t count) {
     P.empty.push_back({(int32_t)q, (int32_t)std::min<int64_t>(kEmptyPiece, first + count - q)});
 }
 
+// Classes of the gathered ids, about equal in the number of triples that
+// gather each: the heaviest ids one by one onto the lightest class, the
+// others by id modulo n_xcd.  Empty when the id space is far larger than the
+// KB (then the class of id a is a % n_xcd).
+static std::vector<uint8_t> id_classes(const LayoutHost &L, int64_t n_ids, int X) {
+  const int64_t n_t = (int64_t)L.col_a.size();
+  if (X <= 1 || n_ids <= 0 || n_ids > 4 * n_t + (int64_t(1) << 20)) return {};
+  std::vector<int32_t> cnt(n_ids, 0);
+  for (int32_t a : L.col_a) ++cnt[a];
+  std::vector<uint8_t> cls(n_ids);
+  const int64_t k_heavy = std::min<int64_t>(n_ids, 65536);
+  std::vector<int32_t> heavy(n_ids);
+  for (int64_t i = 0; i < n_ids; ++i) heavy[i] = (int32_t)i;
+  auto heavier = [&](int32_t x, int32_t y) { return cnt[x] != cnt[y] ? cnt[x] > cnt[y] : x < y; };
+  std::partial_sort(heavy.begin(), heavy.begin() + k_heavy, heavy.end(), heavier);
+  std::vector<char> is_heavy(n_ids, 0);
+  for (int64_t i = 0; i < k_heavy; ++i) is_heavy[heavy[i]] = 1;
+  int64_t load[kMaxXcd] = {};
+  for (int64_t i = 0; i < n_ids; ++i)
+    if (!is_heavy[i]) {
+      cls[i] = (uint8_t)(i % X);
+      load[i % X] += cnt[i];
+    }
+  for (int64_t i = 0; i < k_heavy; ++i) {
+    int best = 0;
+    for (int k = 1; k < X; ++k)
+      if (load[k] < load[best]) best = k;
+    cls[heavy[i]] = (uint8_t)best;
+    load[best] += cnt[heavy[i]];
+  }
+  return cls;
+}
+
 PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
+  PlanOptions o;
+  o.chunk = chunk;
+  o.fan_in = fan_in;
+  o.n_xcd = 1;
+  return plan_layout(L, o);
+}
+
+PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
   PlanHost P;
+  const int32_t chunk = opt.chunk, fan_in = opt.fan_in;
+  const int X = std::max(1, std::min<int>(opt.n_xcd, kMaxXcd));
   P.chunk = chunk;
   P.fan_in = fan_in;
+  P.n_xcd = X;
   const bool weighted = !L.weight.empty();
   const int64_t n_t = (int64_t)L.col_a.size();
-  std::vector<Entry> &S = P.entries;
-  // Triples, at most one marker per triple, chunk-end markers, padding.
-  S.reserve(2 * n_t + n_t / std::max(1, chunk - 1) + chunk + 2);
-  if (weighted) P.weights.reserve(S.capacity());
-  auto marker = [&](int32_t target) {
-    S.push_back({kMarker, target});
-    if (weighted) P.weights.push_back(0.0f);
+
+  // Rows with triples, in row order; the rows between them are empty.
+  struct RowSpan {
+    int32_t row;
+    int64_t beg, end;
   };
+  std::vector<RowSpan> rows;
+  int64_t next_row = 0;
+  for (int64_t beg = 0, end; beg < n_t; beg = end) {
+    const int32_t q = L.row[beg];
+    for (end = beg + 1; end < n_t && L.row[end] == q;) ++end;
+    add_empty(P, next_row, q - next_row);
+    next_row = (int64_t)q + 1;
+    P.max_row_len = std::max(P.max_row_len, end - beg);
+    rows.push_back({q, beg, end});
+  }
+  add_empty(P, next_row, L.rows - next_row);
+
+  // The order in which triples enter the stream: the layout's own, except
+  // inside hub rows of a plan with several lists.
+  std::vector<int32_t> pos(n_t);
+  for (int64_t i = 0; i < n_t; ++i) pos[i] = (int32_t)i;
+  const std::vector<uint8_t> cls_tab = id_classes(L, opt.n_ids_a, X);
+  auto cls_of = [&](int32_t a) -> int {
+    return cls_tab.empty() ? (int)(a % X) : (int)cls_tab[a];
+  };
+
+  // Segments per list: a hub row's class segments first (rows in order),
+  // then whole rows.  `alone`: the segment is its row's only one.
+  struct Seg {
+    int32_t row;
+    int64_t beg, end;  // into pos
+    bool alone, hub;
+  };
+  std::vector<std::vector<Seg>> segs(X);
+  if (X == 1) {
+    for (const RowSpan &r : rows) segs[0].push_back({r.row, r.beg, r.end, true, false});
+  } else {
+    int64_t load[kMaxXcd] = {};
+    std::vector<uint64_t> key;
+    std::vector<const RowSpan *> small;
+    int64_t total = 0;
+    for (const RowSpan &r : rows) {
+      const int64_t len = r.end - r.beg;
+      total += len + 1;
+      if (len < opt.hub_min) {
+        small.push_back(&r);
+        continue;
+      }
+      // (class, gathered id, second operand) or (class, second operand,
+      // gathered id), both below 2^30: one 64-bit key per triple.
+      key.resize(len);
+      for (int64_t i = 0; i < len; ++i) {
+        const int64_t l = r.beg + i;
+        const uint64_t c = (uint64_t)cls_of(L.col_a[l]);
+        const uint64_t x = (uint64_t)(opt.hub_by_a ? L.col_a[l] : L.col_b[l]);
+        const uint64_t y = (uint64_t)(opt.hub_by_a ? L.col_b[l] : L.col_a[l]);
+        key[i] = (c << 60) | (x << 30) | y;
+      }
+      std::vector<int32_t> idx(len);
+      for (int64_t i = 0; i < len; ++i) idx[i] = (int32_t)i;
+      std::stable_sort(idx.begin(), idx.end(),
+                       [&](int32_t u, int32_t v) { return key[u] < key[v]; });
+      for (int64_t i = 0; i < len; ++i) pos[r.beg + i] = (int32_t)(r.beg + idx[i]);
+      // One segment per class present.
+      std::vector<Seg> mine;
+      for (int64_t b0 = r.beg, b1; b0 < r.end; b0 = b1) {
+        const int c = cls_of(L.col_a[pos[b0]]);
+        for (b1 = b0 + 1; b1 < r.end && cls_of(L.col_a[pos[b1]]) == c;) ++b1;
+        mine.push_back({r.row, b0, b1, false, true});
+        load[c] += b1 - b0 + 1;
+      }
+      const bool alone = mine.size() == 1;
+      for (Seg &g : mine) {
+        g.alone = alone;
+        segs[cls_of(L.col_a[pos[g.beg]])].push_back(g);
+      }
+    }
+    // Whole rows: the list of their first gathered id's class while it has
+    // room, else the lightest list, so that every list gets about the same
+    // number of entries.
+    const int64_t target = (total + X - 1) / X;
+    for (const RowSpan *r : small) {
+      const int64_t w = r->end - r->beg + 1;
+      int c = cls_of(L.col_a[r->beg]);
+      if (load[c] + w > target) {
+        for (int k = 0; k < X; ++k)
+          if (load[k] < load[c]) c = k;
+      }
+      segs[c].push_back({r->row, r->beg, r->end, true, false});
+      load[c] += w;
+    }
+  }
+
+  // Each list's stream.  A marker that writes a partial sum gets a pending
+  // slot (row, list, index within the segment's partials); slots are
+  // numbered once every list is built, consecutively per row.
+  struct Pend {
+    int32_t row, list, idx;
+    int64_t at;  // entry within its list's stream
+  };
+  std::vector<Pend> pend;
+  // Hot ids per list: rank[a] = a's rank in the current list's hot set, -1
+  // for the others (reset after each list).
+  std::vector<int32_t> rank;
+  const bool use_hot = opt.max_hot > 0 && opt.n_ids_a > 0 &&
+                       opt.n_ids_a <= 4 * n_t + (int64_t(1) << 20);
+  if (use_hot) rank.assign(opt.n_ids_a, -1);
+  P.hot_begin.assign(1, 0);
+  std::vector<std::vector<Entry>> S(X);
+  std::vector<std::vector<float>> Wt(X);
+  std::vector<std::vector<int32_t>> first_a(X);  // per chunk: first gathered id, or -1
+  std::vector<std::vector<char>> hub_chunk(X);   // per chunk: starts inside a hub segment
+  for (int x = 0; x < X; ++x) {
+    std::vector<Entry> &E = S[x];
+    std::vector<float> &Wv = Wt[x];
+    int64_t est = 0;
+    for (const Seg &g : segs[x]) est += g.end - g.beg + 1;
+    E.reserve(est + est / std::max(1, chunk - 1) + chunk + 2);
+    auto marker = [&](int32_t target) {
+      E.push_back({kMarker, target});
+      if (weighted) Wv.push_back(0.0f);
+    };
+    auto slot_marker = [&](int32_t row, int32_t idx) {
+      pend.push_back({row, x, idx, (int64_t)E.size()});
+      marker(kNoTarget);  // target set when the slots are numbered
+    };
+    // This list's hot ids: the most gathered ones, at least twice each.
+    std::vector<int32_t> hot;
+    if (use_hot) {
+      std::vector<std::pair<int32_t, int32_t>> cnt;  // (count, id) of the list's ids
+      for (const Seg &g : segs[x])
+        for (int64_t p = g.beg; p < g.end; ++p) {
+          const int32_t a = L.col_a[pos[p]];
+          if (rank[a] < 0) {
+            rank[a] = (int32_t)cnt.size();
+            cnt.push_back({0, a});
+          }
+          ++cnt[rank[a]].first;
+        }
+      for (const auto &c : cnt) rank[c.second] = -1;
+      const size_t k = std::min<size_t>(cnt.size(), (size_t)opt.max_hot);
+      auto more = [](const std::pair<int32_t, int32_t> &u, const std::pair<int32_t, int32_t> &v) {
+        return u.first != v.first ? u.first > v.first : u.second < v.second;
+      };
+      std::partial_sort(cnt.begin(), cnt.begin() + k, cnt.end(), more);
+      for (size_t i = 0; i < k && cnt[i].first >= 2; ++i) hot.push_back(cnt[i].second);
+      for (size_t i = 0; i < hot.size(); ++i) rank[hot[i]] = (int32_t)i;
+    }
+    P.hot_ids.insert(P.hot_ids.end(), hot.begin(), hot.end());
+    P.hot_begin.push_back((int64_t)P.hot_ids.size());
+    for (const Seg &g : segs[x]) {
+      int32_t parts = 0;
+      bool pending = false;  // triples of this segment since the last marker
+      int32_t prev_b = 0;
+      for (int64_t p = g.beg; p < g.end; ++p) {
+        if ((int64_t)E.size() % chunk == chunk - 1) {
+          // The chunk's last entry must be a marker.
+          if (pending)
+            slot_marker(g.row, parts++);
+          else
+            marker(kNoTarget);
+          pending = false;
+        }
+        const int32_t l = pos[p];
+        // A run starts after every marker and wherever col_b changes.
+        const bool run_start = !pending || L.col_b[l] != prev_b;
+        const int64_t c = (int64_t)E.size() / chunk;
+        if ((int64_t)first_a[x].size() <= c) {
+          first_a[x].resize(c + 1, -1);
+          hub_chunk[x].resize(c + 1, 0);
+        }
+        if (first_a[x][c] < 0) {
+          first_a[x][c] = L.col_a[l];
+          hub_chunk[x][c] = g.hub;
+        }
+        const int32_t hr = use_hot ? rank[L.col_a[l]] : -1;
+        if (hr >= 0)
+          E.push_back({kHotBase - (hr | (run_start ? kHotRunStart : 0)), L.col_b[l]});
+        else
+          E.push_back({L.col_a[l] | (run_start ? kRunStart : 0), L.col_b[l]});
+        if (weighted) Wv.push_back(L.weight[l]);
+        prev_b = L.col_b[l];
+        pending = true;
+      }
+      if (!g.alone || parts > 0)
+        slot_marker(g.row, parts++);
+      else
+        marker(g.row);
+    }
+    // Pad with no-op markers to whole chunks: every lane group then walks
+    // exactly `chunk` entries.
+    while ((int64_t)E.size() % chunk != 0) marker(kNoTarget);
+    for (int32_t a : hot) rank[a] = -1;
+    first_a[x].resize(E.size() / chunk, -1);
+    hub_chunk[x].resize(E.size() / chunk, 0);
+  }
+
+  // Slots: per row in (list, index) order, rows in row order.
+  std::vector<int32_t> order(pend.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = (int32_t)i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t u, int32_t v) {
+    const Pend &a = pend[u], &b = pend[v];
+    if (a.row != b.row) return a.row < b.row;
+    if (a.list != b.list) return a.list < b.list;
+    return a.idx < b.idx;
+  });
   struct Split {
     int32_t row;
     int64_t first, n;
   };
   std::vector<Split> splits;
-  // The triples come sorted by row; the rows between two rows with triples
-  // (and before the first, after the last) are empty.
-  int64_t next_row = 0;
-  for (int64_t beg = 0, end; beg < n_t; beg = end) {
-    const int64_t q = L.row[beg];
-    for (end = beg + 1; end < n_t && L.row[end] == q;) ++end;
-    add_empty(P, next_row, q - next_row);
-    next_row = q + 1;
-    P.max_row_len = std::max(P.max_row_len, end - beg);
-    int64_t first_slot = -1, n_slots = 0;
-    bool pending = false;  // triples of this row since the last marker
-    for (int64_t p = beg; p < end; ++p) {
-      if ((int64_t)S.size() % chunk == chunk - 1) {
-        // The chunk's last entry must be a marker.
-        if (pending) {
-          if (n_slots == 0) first_slot = P.n_slots;
-          marker(-(int32_t)P.n_slots - 1);
-          ++P.n_slots;
-          ++n_slots;
-        } else {
-          marker(kNoTarget);
-        }
-        pending = false;
-      }
-      // A run starts after every marker and wherever col_b changes.
-      const bool run_start = !pending || L.col_b[p] != L.col_b[p - 1];
-      S.push_back({L.col_a[p] | (run_start ? kRunStart : 0), L.col_b[p]});
-      if (weighted) P.weights.push_back(L.weight[p]);
-      pending = true;
-    }
-    if (n_slots > 0) {
-      marker(-(int32_t)P.n_slots - 1);
+  for (size_t i = 0; i < order.size();) {
+    const int32_t row = pend[order[i]].row;
+    const int64_t first = P.n_slots;
+    size_t j = i;
+    for (; j < order.size() && pend[order[j]].row == row; ++j) {
+      const Pend &q = pend[order[j]];
+      S[q.list][q.at].y = -(int32_t)P.n_slots - 1;
       ++P.n_slots;
-      ++n_slots;
-      splits.push_back({(int32_t)q, first_slot, n_slots});
-      ++P.n_split_rows;
-    } else {
-      marker((int32_t)q);
     }
+    splits.push_back({row, first, (int64_t)(j - i)});
+    ++P.n_split_rows;
+    i = j;
   }
-  add_empty(P, next_row, L.rows - next_row);
-  // Pad with no-op markers to whole chunks: every lane group then walks
-  // exactly `chunk` entries.
-  while ((int64_t)S.size() % chunk != 0) marker(kNoTarget);
-  P.n_chunks = (int64_t)S.size() / chunk;
+
+  // Chunk order inside each list: hub chunks by their first gathered id,
+  // then the others in stream order.
+  P.xcd_chunk.assign(1, 0);
+  for (int x = 0; x < X; ++x) {
+    const int64_t nc = (int64_t)S[x].size() / chunk;
+    std::vector<int64_t> co(nc);
+    for (int64_t c = 0; c < nc; ++c) co[c] = c;
+    if (X > 1 && opt.band)
+      std::stable_sort(co.begin(), co.end(), [&](int64_t u, int64_t v) {
+        const bool hu = hub_chunk[x][u], hv = hub_chunk[x][v];
+        if (hu != hv) return hu;
+        return hu && first_a[x][u] < first_a[x][v];
+      });
+    for (int64_t c : co) {
+      P.entries.insert(P.entries.end(), S[x].begin() + c * chunk, S[x].begin() + (c + 1) * chunk);
+      if (weighted)
+        P.weights.insert(P.weights.end(), Wt[x].begin() + c * chunk,
+                         Wt[x].begin() + (c + 1) * chunk);
+    }
+    std::vector<Entry>().swap(S[x]);
+    std::vector<float>().swap(Wt[x]);
+    P.xcd_chunk.push_back((int64_t)P.entries.size() / chunk);
+  }
+  P.n_chunks = (int64_t)P.entries.size() / chunk;
+
   // Combine levels: a row split into n partials is reduced fan_in slots at a
   // time until one task writes the row.
-  for (const Split &s : splits) {
-    int64_t first_slot = s.first, cnt = s.n;
+  for (const Split &sp : splits) {
+    int64_t first_slot = sp.first, cnt = sp.n;
     size_t level = 0;
     while (cnt > fan_in) {
       const int64_t groups = (cnt + fan_in - 1) / fan_in;
@@ -423,7 +660,7 @@ PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {
       ++level;
     }
     if (P.levels.size() <= level) P.levels.resize(level + 1);
-    P.levels[level].push_back({(int32_t)first_slot, (int32_t)cnt, s.row, 0});
+    P.levels[level].push_back({(int32_t)first_slot, (int32_t)cnt, sp.row, 0});
   }
   return P;
 }

@@ -38,9 +38,12 @@ struct LayoutHost {
 
 // One 8-byte stream entry.  A triple: x = (id gathered for this triple, col_a)
 // | kRunStart when it is the first triple of a run of equal col_b since the
-// last marker, y = col_b.  A marker (x = kMarker): write the running sum to y
-// -- a row (y >= 0), a workspace slot -(y + 1), or nothing (y = kNoTarget) --
-// and restart from zero.
+// last marker, y = col_b.  A triple whose gathered id is one of its chunk
+// list's hot ids (see PlanHost::hot_ids) names the id by its rank in that
+// list instead: x = kHotBase - (rank | kHotRunStart when a run starts), so
+// x <= kHotBase.  A marker (x = kMarker): write the running sum to y -- a
+// row (y >= 0), a workspace slot -(y + 1), or nothing (y = kNoTarget) -- and
+// restart from zero.
 struct Entry {
   int32_t x, y;
 };
@@ -48,6 +51,9 @@ constexpr int32_t kMarker = -1;
 constexpr int32_t kRunStart = 1 << 30;
 constexpr int32_t kIdMask = kRunStart - 1;
 constexpr int32_t kNoTarget = INT32_MIN;
+constexpr int32_t kHotBase = -2;
+constexpr int32_t kHotRunStart = 1 << 20;
+constexpr int32_t kHotRankMask = kHotRunStart - 1;
 
 // The stream plan of one layout.  The sorted triples of every non-empty row
 // are followed by a marker that writes the row, and the stream is cut into
@@ -68,10 +74,43 @@ struct EmptyPiece {
 };
 constexpr int32_t kEmptyPiece = 4096;
 
+// Chunk lists: the stream is cut into n_xcd consecutive lists of whole
+// chunks, list x for the workgroups that run on XCD x (workgroup w runs on
+// XCD w mod 8 on an MI355X), so that each XCD's L2 caches the rows its own
+// triples gather.  The gathered ids are split into n_xcd classes of about
+// equal weight; a row with at least hub_min triples is cut into one segment
+// per class present, each in its class's list (its partial sums go to slots
+// and are combined like those of a row that crosses chunks), and every other
+// row goes whole into one list (the class of its first gathered id, unless
+// that list is already full).  Inside a hub segment the triples are ordered
+// by gathered id (hub_by_a) or by (second operand, gathered id), and a
+// list's hub chunks are ordered by their first gathered id (band), so that
+// the chunks in flight at once gather from nearby rows.  The order of
+// chunks never changes a result: each chunk's sums and targets are fixed.
+constexpr int kMaxXcd = 8;
+struct PlanOptions {
+  int32_t chunk = 256;
+  int32_t fan_in = 32;
+  int32_t n_xcd = 1;       // chunk lists (1: a single list in row order)
+  int64_t hub_min = 256;   // rows with at least this many triples are split by class
+  bool hub_by_a = true;
+  bool band = true;
+  int64_t n_ids_a = 0;     // size of the gathered id space
+  int32_t max_hot = 0;     // hot ids per chunk list (0: none)
+};
+
 struct PlanHost {
   int32_t chunk = 0;
   int32_t fan_in = 0;
   int64_t n_chunks = 0;
+  int32_t n_xcd = 1;
+  std::vector<int64_t> xcd_chunk;   // n_xcd + 1 boundaries of the chunk lists
+  // Per chunk list, its most gathered ids (at most max_hot, each gathered at
+  // least twice by the list's triples), most gathered first: list x's are
+  // hot_ids[hot_begin[x] .. hot_begin[x + 1]).  The kernels keep the rows of
+  // as many of them as fit in LDS and read the others' ids from LDS.
+  std::vector<int32_t> hot_ids;
+  std::vector<int64_t> hot_begin;   // n_xcd + 1 boundaries
   std::vector<Entry> entries;
   std::vector<float> weights;       // per entry (markers 0), empty for a hard KB
   std::vector<EmptyPiece> empty;    // the rows no triple reaches
@@ -101,7 +140,10 @@ void build_layouts(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                    const float *weight, bool keep_perm, bool keep_offsets, LayoutHost out[3],
                    LayoutSort how = LayoutSort::kAuto);
 
-// Cuts a layout into chunks, marks the flush points and plans the combine levels.
+// Cuts a layout into chunk lists, marks the flush points and plans the
+// combine levels.
+PlanHost plan_layout(const LayoutHost &layout, const PlanOptions &options);
+// One list in row order (n_xcd = 1).
 PlanHost plan_layout(const LayoutHost &layout, int32_t chunk, int32_t fan_in);
 
 }  // namespace kbf

@@ -43,7 +43,7 @@ static void check_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk, co
         if (slot >= 0 && slot < P.n_slots) ++slot_written[slot];
       }
     } else {
-      CHECK(e.x >= 0, "%s: entry %lld", what, (long long)p);
+      CHECK(e.x >= 0 || e.x <= kHotBase, "%s: entry %lld", what, (long long)p);
       ++triples;
     }
   }
@@ -89,6 +89,91 @@ static void check_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk, co
   if (!P.weights.empty()) CHECK(P.weights.size() == P.entries.size(), "%s: weights", what);
 }
 
+// Runs the plan on the CPU with an exact integer value per triple, chunk by
+// chunk as the stream kernel does (a run's second operand is taken from its
+// first triple), then the combine levels in order, and compares every row's
+// total with a direct sum over the layout: each triple counted once, into its
+// own row, whatever the lists and the chunk order.
+static void interpret_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk,
+                           const char *what) {
+  auto val = [](int32_t a, int32_t b) -> int64_t {
+    return (int64_t)(a % 1009) * 1013 + (int64_t)(b % 997) + 1;
+  };
+  std::vector<int64_t> want(L.rows, 0), got(L.rows, 0), slot(P.n_slots, 0);
+  std::vector<int> writes(L.rows, 0);
+  for (size_t p = 0; p < L.col_a.size(); ++p) want[L.row[p]] += val(L.col_a[p], L.col_b[p]);
+  CHECK((int64_t)P.xcd_chunk.size() == P.n_xcd + 1 && P.xcd_chunk.front() == 0 &&
+            P.xcd_chunk.back() == P.n_chunks,
+        "%s: chunk lists", what);
+  for (size_t x = 1; x < P.xcd_chunk.size(); ++x)
+    CHECK(P.xcd_chunk[x - 1] <= P.xcd_chunk[x], "%s: chunk list %zu", what, x);
+  const bool hot = !P.hot_begin.empty();
+  CHECK(!hot || ((int64_t)P.hot_begin.size() == P.n_xcd + 1 && P.hot_begin.front() == 0 &&
+                 P.hot_begin.back() == (int64_t)P.hot_ids.size()),
+        "%s: hot id lists", what);
+  int list = 0;
+  for (int64_t c = 0; c < P.n_chunks; ++c) {
+    while (list + 1 < (int)P.xcd_chunk.size() - 1 && c >= P.xcd_chunk[list + 1]) ++list;
+    int64_t acc = 0;
+    bool held = false;
+    int32_t hb = 0;
+    for (int64_t p = c * chunk; p < (c + 1) * chunk; ++p) {
+      const Entry &e = P.entries[p];
+      if (e.x >= 0 || e.x <= kHotBase) {
+        int32_t a;
+        bool start;
+        if (e.x >= 0) {
+          a = e.x & kIdMask;
+          start = (e.x & kRunStart) != 0;
+        } else {
+          const int32_t v = kHotBase - e.x;
+          const int64_t r = v & kHotRankMask;
+          start = (v & kHotRunStart) != 0;
+          const bool ok = hot && r < P.hot_begin[list + 1] - P.hot_begin[list];
+          CHECK(ok, "%s: hot rank %lld outside list %d", what, (long long)r, list);
+          a = ok ? P.hot_ids[P.hot_begin[list] + r] : 0;
+        }
+        if (start) {
+          hb = e.y;
+          held = true;
+        }
+        CHECK(held && hb == e.y, "%s: entry %lld outside a run of its second operand", what,
+              (long long)p);
+        acc += val(a, e.y);
+      } else {
+        if (e.y >= 0 && e.y < L.rows) {
+          got[e.y] += acc;
+          ++writes[e.y];
+        } else if (e.y != kNoTarget && -(int64_t)e.y - 1 < P.n_slots) {
+          slot[-(int64_t)e.y - 1] = acc;
+        }
+        acc = 0;
+        held = false;
+      }
+    }
+  }
+  for (const auto &level : P.levels)
+    for (const CombineTask &t : level) {
+      int64_t sum = 0;
+      for (int32_t i = 0; i < t.n; ++i)
+        if (t.first + i < P.n_slots) sum += slot[t.first + i];
+      if (t.dst >= 0 && t.dst < L.rows) {
+        got[t.dst] += sum;
+        ++writes[t.dst];
+      } else if (t.dst < 0 && -(int64_t)t.dst - 1 < P.n_slots) {
+        slot[-(int64_t)t.dst - 1] = sum;
+      }
+    }
+  std::vector<char> has(L.rows, 0);
+  for (int32_t q : L.row) has[q] = 1;
+  for (int64_t q = 0; q < L.rows; ++q) {
+    CHECK(got[q] == want[q], "%s: row %lld sums to %lld, want %lld", what, (long long)q,
+          (long long)got[q], (long long)want[q]);
+    CHECK(writes[q] == (has[q] ? 1 : 0), "%s: row %lld written %d times", what, (long long)q,
+          writes[q]);
+  }
+}
+
 static void check_layout(const LayoutHost &L, int64_t n_t, const char *what) {
   CHECK((int64_t)L.col_a.size() == n_t && (int64_t)L.col_b.size() == n_t &&
             (int64_t)L.row.size() == n_t,
@@ -129,7 +214,28 @@ static void run_case(const char *what, int64_t n_e, int64_t n_r, std::vector<int
           "%s: layout %d differs between the radix and the counting sorts", what, k);
     check_layout(L[k], n_t, what);
     for (int32_t chunk : {16, 24, 256}) {
-      for (int32_t fan_in : {2, 3, 32}) check_plan(L[k], plan_layout(L[k], chunk, fan_in), chunk, what);
+      for (int32_t fan_in : {2, 3, 32}) {
+        const PlanHost P = plan_layout(L[k], chunk, fan_in);
+        check_plan(L[k], P, chunk, what);
+        interpret_plan(L[k], P, chunk, what);
+      }
+      // One chunk list per XCD, hub rows split by class of the gathered id.
+      for (int64_t hub_min : {int64_t(4), int64_t(64)})
+        for (bool by_a : {true, false})
+          for (bool band : {true, false}) {
+            PlanOptions po;
+            po.chunk = chunk;
+            po.fan_in = 3;
+            po.n_xcd = 8;
+            po.hub_min = hub_min;
+            po.hub_by_a = by_a;
+            po.band = band;
+            po.n_ids_a = n_e;
+            po.max_hot = band ? 7 : 0;
+            const PlanHost P = plan_layout(L[k], po);
+            check_plan(L[k], P, chunk, what);
+            interpret_plan(L[k], P, chunk, what);
+          }
     }
   }
 }
