@@ -491,13 +491,6 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
     int64_t at;  // entry within its list's stream
   };
   std::vector<Pend> pend;
-  // Hot ids per list: rank[a] = a's rank in the current list's hot set, -1
-  // for the others (reset after each list).
-  std::vector<int32_t> rank;
-  const bool use_hot = opt.max_hot > 0 && opt.n_ids_a > 0 &&
-                       opt.n_ids_a <= 4 * n_t + (int64_t(1) << 20);
-  if (use_hot) rank.assign(opt.n_ids_a, -1);
-  P.hot_begin.assign(1, 0);
   std::vector<std::vector<Entry>> S(X);
   std::vector<std::vector<float>> Wt(X);
   std::vector<std::vector<int32_t>> first_a(X);  // per chunk: first gathered id, or -1
@@ -516,30 +509,6 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
       pend.push_back({row, x, idx, (int64_t)E.size()});
       marker(kNoTarget);  // target set when the slots are numbered
     };
-    // This list's hot ids: the most gathered ones, at least twice each.
-    std::vector<int32_t> hot;
-    if (use_hot) {
-      std::vector<std::pair<int32_t, int32_t>> cnt;  // (count, id) of the list's ids
-      for (const Seg &g : segs[x])
-        for (int64_t p = g.beg; p < g.end; ++p) {
-          const int32_t a = L.col_a[pos[p]];
-          if (rank[a] < 0) {
-            rank[a] = (int32_t)cnt.size();
-            cnt.push_back({0, a});
-          }
-          ++cnt[rank[a]].first;
-        }
-      for (const auto &c : cnt) rank[c.second] = -1;
-      const size_t k = std::min<size_t>(cnt.size(), (size_t)opt.max_hot);
-      auto more = [](const std::pair<int32_t, int32_t> &u, const std::pair<int32_t, int32_t> &v) {
-        return u.first != v.first ? u.first > v.first : u.second < v.second;
-      };
-      std::partial_sort(cnt.begin(), cnt.begin() + k, cnt.end(), more);
-      for (size_t i = 0; i < k && cnt[i].first >= 2; ++i) hot.push_back(cnt[i].second);
-      for (size_t i = 0; i < hot.size(); ++i) rank[hot[i]] = (int32_t)i;
-    }
-    P.hot_ids.insert(P.hot_ids.end(), hot.begin(), hot.end());
-    P.hot_begin.push_back((int64_t)P.hot_ids.size());
     for (const Seg &g : segs[x]) {
       int32_t parts = 0;
       bool pending = false;  // triples of this segment since the last marker
@@ -565,11 +534,7 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
           first_a[x][c] = L.col_a[l];
           hub_chunk[x][c] = g.hub;
         }
-        const int32_t hr = use_hot ? rank[L.col_a[l]] : -1;
-        if (hr >= 0)
-          E.push_back({kHotBase - (hr | (run_start ? kHotRunStart : 0)), L.col_b[l]});
-        else
-          E.push_back({L.col_a[l] | (run_start ? kRunStart : 0), L.col_b[l]});
+        E.push_back({L.col_a[l] | (run_start ? kRunStart : 0), L.col_b[l]});
         if (weighted) Wv.push_back(L.weight[l]);
         prev_b = L.col_b[l];
         pending = true;
@@ -582,7 +547,6 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
     // Pad with no-op markers to whole chunks: every lane group then walks
     // exactly `chunk` entries.
     while ((int64_t)E.size() % chunk != 0) marker(kNoTarget);
-    for (int32_t a : hot) rank[a] = -1;
     first_a[x].resize(E.size() / chunk, -1);
     hub_chunk[x].resize(E.size() / chunk, 0);
   }

@@ -38,12 +38,9 @@ struct LayoutHost {
 
 // One 8-byte stream entry.  A triple: x = (id gathered for this triple, col_a)
 // | kRunStart when it is the first triple of a run of equal col_b since the
-// last marker, y = col_b.  A triple whose gathered id is one of its chunk
-// list's hot ids (see PlanHost::hot_ids) names the id by its rank in that
-// list instead: x = kHotBase - (rank | kHotRunStart when a run starts), so
-// x <= kHotBase.  A marker (x = kMarker): write the running sum to y -- a
-// row (y >= 0), a workspace slot -(y + 1), or nothing (y = kNoTarget) -- and
-// restart from zero.
+// last marker, y = col_b.  A marker (x = kMarker): write the running sum to y
+// -- a row (y >= 0), a workspace slot -(y + 1), or nothing (y = kNoTarget) --
+// and restart from zero.
 struct Entry {
   int32_t x, y;
 };
@@ -51,9 +48,6 @@ constexpr int32_t kMarker = -1;
 constexpr int32_t kRunStart = 1 << 30;
 constexpr int32_t kIdMask = kRunStart - 1;
 constexpr int32_t kNoTarget = INT32_MIN;
-constexpr int32_t kHotBase = -2;
-constexpr int32_t kHotRunStart = 1 << 20;
-constexpr int32_t kHotRankMask = kHotRunStart - 1;
 
 // The stream plan of one layout.  The sorted triples of every non-empty row
 // are followed by a marker that writes the row, and the stream is cut into
@@ -96,7 +90,6 @@ struct PlanOptions {
   bool hub_by_a = true;
   bool band = true;
   int64_t n_ids_a = 0;     // size of the gathered id space
-  int32_t max_hot = 0;     // hot ids per chunk list (0: none)
 };
 
 struct PlanHost {
@@ -105,12 +98,6 @@ struct PlanHost {
   int64_t n_chunks = 0;
   int32_t n_xcd = 1;
   std::vector<int64_t> xcd_chunk;   // n_xcd + 1 boundaries of the chunk lists
-  // Per chunk list, its most gathered ids (at most max_hot, each gathered at
-  // least twice by the list's triples), most gathered first: list x's are
-  // hot_ids[hot_begin[x] .. hot_begin[x + 1]).  The kernels keep the rows of
-  // as many of them as fit in LDS and read the others' ids from LDS.
-  std::vector<int32_t> hot_ids;
-  std::vector<int64_t> hot_begin;   // n_xcd + 1 boundaries
   std::vector<Entry> entries;
   std::vector<float> weights;       // per entry (markers 0), empty for a hard KB
   std::vector<EmptyPiece> empty;    // the rows no triple reaches

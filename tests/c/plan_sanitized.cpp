@@ -43,7 +43,7 @@ static void check_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk, co
         if (slot >= 0 && slot < P.n_slots) ++slot_written[slot];
       }
     } else {
-      CHECK(e.x >= 0 || e.x <= kHotBase, "%s: entry %lld", what, (long long)p);
+      CHECK(e.x >= 0, "%s: entry %lld", what, (long long)p);
       ++triples;
     }
   }
@@ -107,33 +107,15 @@ static void interpret_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk
         "%s: chunk lists", what);
   for (size_t x = 1; x < P.xcd_chunk.size(); ++x)
     CHECK(P.xcd_chunk[x - 1] <= P.xcd_chunk[x], "%s: chunk list %zu", what, x);
-  const bool hot = !P.hot_begin.empty();
-  CHECK(!hot || ((int64_t)P.hot_begin.size() == P.n_xcd + 1 && P.hot_begin.front() == 0 &&
-                 P.hot_begin.back() == (int64_t)P.hot_ids.size()),
-        "%s: hot id lists", what);
-  int list = 0;
   for (int64_t c = 0; c < P.n_chunks; ++c) {
-    while (list + 1 < (int)P.xcd_chunk.size() - 1 && c >= P.xcd_chunk[list + 1]) ++list;
     int64_t acc = 0;
     bool held = false;
     int32_t hb = 0;
     for (int64_t p = c * chunk; p < (c + 1) * chunk; ++p) {
       const Entry &e = P.entries[p];
-      if (e.x >= 0 || e.x <= kHotBase) {
-        int32_t a;
-        bool start;
-        if (e.x >= 0) {
-          a = e.x & kIdMask;
-          start = (e.x & kRunStart) != 0;
-        } else {
-          const int32_t v = kHotBase - e.x;
-          const int64_t r = v & kHotRankMask;
-          start = (v & kHotRunStart) != 0;
-          const bool ok = hot && r < P.hot_begin[list + 1] - P.hot_begin[list];
-          CHECK(ok, "%s: hot rank %lld outside list %d", what, (long long)r, list);
-          a = ok ? P.hot_ids[P.hot_begin[list] + r] : 0;
-        }
-        if (start) {
+      if (e.x >= 0) {
+        const int32_t a = e.x & kIdMask;
+        if (e.x & kRunStart) {
           hb = e.y;
           held = true;
         }
@@ -231,7 +213,6 @@ static void run_case(const char *what, int64_t n_e, int64_t n_r, std::vector<int
             po.hub_by_a = by_a;
             po.band = band;
             po.n_ids_a = n_e;
-            po.max_hot = band ? 7 : 0;
             const PlanHost P = plan_layout(L[k], po);
             check_plan(L[k], P, chunk, what);
             interpret_plan(L[k], P, chunk, what);
