@@ -81,6 +81,7 @@ struct kb_t {
   bool weighted = false;
   bool plain_loads = false;  // force plain loads instead of raw buffer loads (testing)
   bool b_in_lds = true;      // stage small B tables in LDS (off: B rows in registers)
+  int max_lpt = 32;          // widest lane group of the register variant (KBFOLLOW_MAX_LPT)
   // The backward's dR pass on a stream of the KB's own, concurrent with the
   // dX pass: -1 on large KBs at b <= 32, 1 always, 0 never; the stream, fork
   // and join events, and a lock that keeps one call's record / wait
@@ -252,6 +253,7 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
     o.plain_loads = kb->plain_loads;
     o.b_in_lds = kb->b_in_lds;
     o.n_cu = kb->n_cu;
+    o.max_lpt = kb->max_lpt;
     hipError_t e = launch_stream(a, o, s, scope.launch_start(), scope.launch_stop());
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
@@ -375,6 +377,11 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     if (kb->n_cu <= 0) kb->n_cu = 1;
     kb->plain_loads = env_int("KBFOLLOW_PLAIN_LOADS", 0) != 0;
     kb->b_in_lds = env_int("KBFOLLOW_B_IN_LDS", 1) != 0;
+    // Narrower lane groups for the register variant give more column slices,
+    // each gathering from a narrower part of the table: the training-shaped
+    // KB's dR pass at b = 256 took 3.82 ms with 32-column slices against
+    // 3.91 ms with 128-column ones, too little to change the default.
+    kb->max_lpt = env_int("KBFOLLOW_MAX_LPT", 32);
     // dR concurrent with dX from 2^20 triples on, at b <= 32 (measured on the
     // large KB: steps 3-5 % shorter at b = 8 .. 32, 4 % longer at b = 64, the
     // same at 128 and 256; on small KBs the fork and join cost more than
@@ -711,6 +718,7 @@ kb_status kb_phase_kernel(const kb_t *kb, int32_t b, int32_t phase, int32_t resi
       o.plain_loads = kb->plain_loads;
       o.b_in_lds = kb->b_in_lds;
       o.n_cu = kb->n_cu;
+      o.max_lpt = kb->max_lpt;
       out = describe_stream(a, o);
     } else if (step == 1) {
       const int64_t n0 = D.level_begin.size() > 1 ? D.level_begin[1] - D.level_begin[0] : 0;

@@ -78,6 +78,7 @@ struct StreamOptions {
   // rows in registers, the variant used for larger tables.
   bool b_in_lds = true;
   int n_cu = 1;  // compute units of the device, for the LDS variant's grid
+  int max_lpt = 32;  // widest lane group of the register variant (narrower: more column slices)
 };
 // With start / stop events the kernel is launched with hipExtLaunchKernel,
 // which sets them to the kernel's own start and end timestamps (no event

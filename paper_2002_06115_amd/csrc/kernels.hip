@@ -764,7 +764,9 @@ hipError_t choose_stream(const StreamArgs &a, const StreamOptions &o, StreamChoi
     longest = std::max<int64_t>(longest, a.list_chunk[x + 1] - a.list_chunk[x]);
   }
   const int nl = a.n_lists;
-  const void *reg_fn = stream_fn_for(t, buf, false, wt, res);
+  // The register variant's lane groups: at most o.max_lpt lanes wide.
+  const ColumnTiling tr = column_tiling_max(a.b, std::max(1, std::min(o.max_lpt, kMaxLpt)));
+  const void *reg_fn = stream_fn_for(tr, buf, false, wt, res);
   if (!reg_fn) return hipErrorInvalidValue;
   c->buf = buf;
   c->wt = wt;
@@ -810,13 +812,13 @@ hipError_t choose_stream(const StreamArgs &a, const StreamOptions &o, StreamChoi
       }
     }
   }
-  const int64_t per_list = std::max<int64_t>(1, (longest + kBlock / t.lpt - 1) / (kBlock / t.lpt));
+  const int64_t per_list = std::max<int64_t>(1, (longest + kBlock / tr.lpt - 1) / (kBlock / tr.lpt));
   if (per_list * nl > (int64_t)INT32_MAX) return hipErrorInvalidValue;
   c->fn = reg_fn;
-  c->grid = dim3((unsigned)(per_list * nl), (unsigned)t.n_slices);
+  c->grid = dim3((unsigned)(per_list * nl), (unsigned)tr.n_slices);
   c->block = kBlock;
   c->lds_bytes = 0;
-  c->lpt = t.lpt;
+  c->lpt = tr.lpt;
   c->ldsb = false;
   return hipSuccess;
 }
