@@ -389,6 +389,11 @@ def seeds_of(w, extra=None):
 
 def follow_bench(args, torch, kbgen, kbf):
     w = kbgen.WORKLOADS[args.workload]
+    if args.batch:
+        # The same KB; inputs are drawn per example, so the first columns
+        # are those of the default width.
+        import dataclasses
+        w = dataclasses.replace(w, batch=int(args.batch))
     t0 = time.perf_counter()
     kb = kbgen.make_kb(w)
     X_bm, R_bm, dY_bm = kbgen.make_x(w), kbgen.make_r(w), kbgen.make_dy(w)
@@ -739,6 +744,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="large",
                     help="tiny | metaqa | chain3 | large | train (kbgen workload names)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="batch width b instead of the workload's own (the same KB)")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="host threads for the oracle (0: the cores this process may use, "
                          "at most 16)")

@@ -81,7 +81,8 @@ struct kb_t {
   bool weighted = false;
   bool plain_loads = false;  // force plain loads instead of raw buffer loads (testing)
   bool b_in_lds = true;      // stage small B tables in LDS (off: B rows in registers)
-  int max_lpt = 32;          // widest lane group of the register variant (KBFOLLOW_MAX_LPT)
+  bool stream_stamps = true; // time stream kernels by their dispatch timestamps (off: event records)
+  int max_lpt = 0;           // widest lane group of the register variant; 0: per pass (lane_cap)
   // The backward's dR pass on a stream of the KB's own, concurrent with the
   // dX pass: -1 on large KBs at b <= 32, 1 always, 0 never; the stream, fork
   // and join events, and a lock that keeps one call's record / wait
@@ -232,6 +233,19 @@ kb_status check_device(const kb_t *kb) {
   return KB_OK;
 }
 
+// The widest lane group of the register variant for a pass.  Narrower lane
+// groups mean more column slices, each gathering from a narrower part of the
+// table and re-reading the entry stream.  That pays for the dR pass (B = X,
+// read in registers) at b >= 128: 32-column slices took the training-shaped
+// KB's dR from 3.92 to 3.80 ms at b = 256, the 10 M-entity KB's from 3.51 to
+// 3.42 ms at b = 128 and the MetaQA-shaped KB's from 0.0182 to 0.0175 ms,
+// while at b = 64 they cost 1 % and the forward and dX register variants at
+// b = 128 and 256 lost 12-15 %.
+int lane_cap(const kb_t *kb, int ph_base, int32_t b) {
+  if (kb->max_lpt > 0) return kb->max_lpt;
+  return (ph_base == KB_PH_DR_STREAM && b >= 128) ? 8 : 32;
+}
+
 // Runs one pass: the stream kernel, the first combine level together with
 // the empty rows, the further combine levels.  With Z non-null (one row per
 // output row; A itself for the residual hop, out itself to add in place)
@@ -244,7 +258,7 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
   if (D.n > 0) {
     // Timed by the kernel's own timestamps: no event packets between this
     // launch and the next, which would hold back a concurrent pass.
-    PhaseScope scope(kb, ph_base + 0, s, false);
+    PhaseScope scope(kb, ph_base + 0, s, !kb->stream_stamps);
     StreamArgs a{D.entries, D.weights, D.n, D.chunk, A,           A_rows,     B,
                  B_rows,    b,         out,  D.rows,  slots, D.n_slots, Z ? 1 : 0, gamma, Z,
                  D.n_lists, {}};
@@ -253,7 +267,7 @@ kb_status run_pass(const kb_t *kb, const DevLayout &D, int ph_base, const float 
     o.plain_loads = kb->plain_loads;
     o.b_in_lds = kb->b_in_lds;
     o.n_cu = kb->n_cu;
-    o.max_lpt = kb->max_lpt;
+    o.max_lpt = lane_cap(kb, ph_base, b);
     hipError_t e = launch_stream(a, o, s, scope.launch_start(), scope.launch_stop());
     if (e != hipSuccess) return hip_fail(e, "stream kernel launch");
   }
@@ -377,11 +391,8 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     if (kb->n_cu <= 0) kb->n_cu = 1;
     kb->plain_loads = env_int("KBFOLLOW_PLAIN_LOADS", 0) != 0;
     kb->b_in_lds = env_int("KBFOLLOW_B_IN_LDS", 1) != 0;
-    // Narrower lane groups for the register variant give more column slices,
-    // each gathering from a narrower part of the table: the training-shaped
-    // KB's dR pass at b = 256 took 3.82 ms with 32-column slices against
-    // 3.91 ms with 128-column ones, too little to change the default.
-    kb->max_lpt = env_int("KBFOLLOW_MAX_LPT", 32);
+    kb->stream_stamps = env_int("KBFOLLOW_STREAM_STAMPS", 1) != 0;
+    kb->max_lpt = env_int("KBFOLLOW_MAX_LPT", 0);
     // dR concurrent with dX from 2^20 triples on, at b <= 32 (measured on the
     // large KB: steps 3-5 % shorter at b = 8 .. 32, 4 % longer at b = 64, the
     // same at 128 and 256; on small KBs the fork and join cost more than
@@ -718,7 +729,7 @@ kb_status kb_phase_kernel(const kb_t *kb, int32_t b, int32_t phase, int32_t resi
       o.plain_loads = kb->plain_loads;
       o.b_in_lds = kb->b_in_lds;
       o.n_cu = kb->n_cu;
-      o.max_lpt = kb->max_lpt;
+      o.max_lpt = lane_cap(kb, pass * 3, b);
       out = describe_stream(a, o);
     } else if (step == 1) {
       const int64_t n0 = D.level_begin.size() > 1 ? D.level_begin[1] - D.level_begin[0] : 0;
