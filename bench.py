@@ -609,6 +609,34 @@ def chain_bench(args, torch, kbgen, kbf):
         [d.t().contiguous().cpu().numpy() for d in res[2]]
     log(f"[chain3] {ms_step:.4f} ms/step, {value:.3e} triple*batch/s")
 
+    # The same step captured into one HIP graph and replayed: no host work
+    # between the ~40 launches.  Every replay must reproduce the eager
+    # step's loss and gradients bit for bit.
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        gres = step()
+    torch.cuda.synchronize()
+    same = []
+    for _ in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        same.append(bool(torch.equal(gres[0], res[0]) and torch.equal(gres[1], res[1]) and
+                         all(torch.equal(a, c) for a, c in zip(gres[2], res[2]))))
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(args.steps):
+        g.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    graph_ms = t0.elapsed_time(t1) / args.steps
+    del g
+    log(f"[chain3] graph replay {graph_ms:.4f} ms/step, bitwise equal to eager: {same}")
+
     cpu, parity = None, None
     if not args.no_cpu_baseline:
         from oracle import chain as ochain
@@ -647,6 +675,9 @@ def chain_bench(args, torch, kbgen, kbf):
         "seeds": seeds_of(w), "kb_sha256": kb.sha256(), "kb_stats": kb.stats(),
         "phases_ms_per_step": {k: round(v[0], 4) for k, v in phases.items()},
         "kernel_ms_per_step": {k: round(v, 4) for k, v in share.items()},
+        "graph": {"ms_per_step": round(graph_ms, 4),
+                  "triple_batch_per_s": hops * kb.n_triples * b / (graph_ms * 1e-3),
+                  "replays_bitwise_equal_to_eager": all(same)},
         "roofline": {"bound": "latency", "achieved": None, "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": None, "traffic": None,
                      "note": "a 1 k-entity KB: each launch moves a few MB at most; the step is "

@@ -22,8 +22,9 @@
  * Streams and memory: every call only enqueues work on `stream` (hipStream_t,
  * NULL = null stream), allocates nothing and returns.  All pointers are
  * DEVICE pointers; input and output arrays must not overlap unless stated.
- * The kernels are sized for chain-harness shapes: one workgroup reduces 64
- * columns over all n rows.
+ * The kernels are sized for chain-harness shapes: one 1024-thread workgroup
+ * reduces 16 columns over all n rows (64 rows at a time, four deep in
+ * flight), so a launch spans ceil(b / 16) workgroups.
  *
  * Errors: arguments are checked before anything is enqueued; on failure
  * nothing is launched.  Returns KBC_OK, KBC_EINVAL (null pointer, n < 1 or

@@ -5,7 +5,7 @@ Host: libkbchain.so exports every entry point the header declares and
 rejects bad arguments before launching anything.  GPU: every operation
 against a float64 numpy evaluation of its formula (the softmax of the chain
 oracle, oracle/chain.py, for the forward softmax), on column counts that are
-and are not multiples of the 64-column tile and on row counts from 1 up, and
+and are not multiples of the 16-column tile and on row counts from 1 up, and
 bitwise reproducibility.
 """
 import ctypes
@@ -48,7 +48,8 @@ def test_bad_arguments_are_refused_before_any_launch():
     assert lib.kbc_softmax_xent(4, 4, d, d, d, None, d, None) == 1
 
 
-SHAPES = [(1, 1), (7, 63), (18, 64), (1000, 65), (43, 130), (50_000, 3)]
+SHAPES = [(1, 1), (7, 15), (18, 16), (1000, 17), (300, 64), (1000, 256), (43, 130), (3, 1100),
+          (50_000, 3)]
 
 
 @pytest.fixture(scope="module")
