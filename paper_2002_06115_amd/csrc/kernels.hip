@@ -61,10 +61,13 @@ constexpr int kFillPieces = 4;
 constexpr int kFillBatch = 4;
 static_assert(kChunkQuantum % kUnroll == 0, "a chunk is a whole number of steps");
 
-// Buffer-resource word 3 for gfx9-family raw buffers, and an offset past any
-// buffer this library makes: such a load returns zeros without touching memory.
+// Buffer-resource word 3 for gfx9-family buffers, and an offset past any raw
+// buffer this library makes (such a load returns zeros without touching
+// memory; tables are at most this many bytes).
 constexpr int kRawBufferWord3 = 0x00020000;
 constexpr uint32_t kOutOfRange = 0xFFFFFFF0u;
+// Largest record stride of a buffer descriptor (a 14-bit field), in bytes.
+constexpr uint64_t kMaxStride = 16383;
 
 // Checked builds (KBFOLLOW_CHECKED) validate every row, slot and combine
 // index before it is used: KBF_CHECKED(i, n) is i when 0 <= i < n, else 0 (a
@@ -120,6 +123,38 @@ __device__ __forceinline__ void load_row(const float *__restrict__ p, float (&v)
   }
 }
 
+typedef float native_float4 __attribute__((ext_vector_type(4)));
+
+// Structured-buffer loads (LLVM's amdgcn struct buffer load intrinsics): the
+// bytes at `off` of record `idx` of a descriptor whose records are `stride`
+// bytes apart.  A record index at or past the descriptor's record count
+// returns zeros without a memory access, so a gathered row needs no multiply
+// for its address and a marker's index (bit 31 set) needs no select.
+__device__ native_float4 struct_buffer_load_f32x4(__amdgpu_buffer_rsrc_t rsrc, int idx, int off,
+                                                  int soff, int aux)
+    __asm("llvm.amdgcn.struct.ptr.buffer.load.v4f32");
+__device__ float struct_buffer_load_f32(__amdgpu_buffer_rsrc_t rsrc, int idx, int off, int soff,
+                                        int aux) __asm("llvm.amdgcn.struct.ptr.buffer.load.f32");
+
+// Record index that no table of this library reaches.
+constexpr uint32_t kNoRecord = 0xFFFFFFFFu;
+
+// VEC floats at byte `off` of record `idx` of a structured buffer (zeros when
+// idx is past its last record).
+template <int VEC>
+__device__ __forceinline__ void gather_row(__amdgpu_buffer_rsrc_t rsrc, uint32_t idx,
+                                           uint32_t off, float (&v)[VEC]) {
+  if constexpr (VEC == 4) {
+    const native_float4 t = struct_buffer_load_f32x4(rsrc, (int)idx, (int)off, 0, 0);
+    v[0] = t[0];
+    v[1] = t[1];
+    v[2] = t[2];
+    v[3] = t[3];
+  } else {
+    v[0] = struct_buffer_load_f32(rsrc, (int)idx, (int)off, 0, 0);
+  }
+}
+
 // VEC floats at byte offset `off` of a raw buffer (zeros when off is past its end).
 template <int VEC>
 __device__ __forceinline__ void load_row_buffer(__amdgpu_buffer_rsrc_t rsrc, uint32_t off,
@@ -134,8 +169,6 @@ __device__ __forceinline__ void load_row_buffer(__amdgpu_buffer_rsrc_t rsrc, uin
     v[0] = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)off, 0, 0));
   }
 }
-
-typedef float native_float4 __attribute__((ext_vector_type(4)));
 
 // VEC floats of LDS at p (16-byte aligned when VEC = 4).
 template <int VEC>
@@ -287,8 +320,18 @@ stream_kernel(StreamArgs a) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, (int)(uint32_t)bytes,
                                              kRawBufferWord3);
   };
-  const __amdgpu_buffer_rsrc_t arsrc = rsrc(a.A, (uint64_t)a.A_rows * row_bytes);
-  const __amdgpu_buffer_rsrc_t brsrc = rsrc(a.B, (uint64_t)a.B_rows * row_bytes);
+  // A and B are gathered by row: structured buffers of row_bytes records
+  // (row_bytes is at most kMaxStride with BUF).  The residual variants keep
+  // raw byte offsets, which measured faster there (their marker rows read
+  // A too, so the record index needs a select either way, and the struct
+  // addresses cost them registers).
+  auto rows_rsrc = [&](const void *p, int64_t rows) {
+    return RES ? rsrc(p, (uint64_t)rows * row_bytes)
+               : __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)row_bytes,
+                                                   (int)rows, kRawBufferWord3);
+  };
+  const __amdgpu_buffer_rsrc_t arsrc = rows_rsrc(a.A, a.A_rows);
+  const __amdgpu_buffer_rsrc_t brsrc = rows_rsrc(a.B, a.B_rows);
   const __amdgpu_buffer_rsrc_t orsrc = rsrc(a.out, (uint64_t)a.out_rows * row_bytes);
   const __amdgpu_buffer_rsrc_t srsrc =
       rsrc(a.slots, (uint64_t)a.n_slots * a.b * sizeof(double));
@@ -376,7 +419,19 @@ stream_kernel(StreamArgs a) {
         // A marker that writes row j of a residual pass reads A[j] for gamma * A[j].
         const bool res_row = RES && !triple && e[u].y >= 0;
         const uint32_t ia = triple ? (uint32_t)(e[u].x & kIdMask) : (uint32_t)e[u].y;
-        if constexpr (BUF) {
+        if constexpr (BUF && !RES) {
+          // A triple's record is its id; a marker's x (-1) with the run-start
+          // bit cleared is past every table, so it reads zeros.
+#if defined(KBFOLLOW_CHECKED)
+          const uint32_t ra = triple ? (uint32_t)KBF_CHECKED(ia, a.A_rows) : kNoRecord;
+#else
+          const uint32_t ra = (uint32_t)e[u].x & ~(uint32_t)kRunStart;
+#endif
+          gather_row<VEC>(arsrc, ra, col_bytes, xa[u]);
+          if constexpr (!LDSB)
+            gather_row<VEC>(brsrc, run_start ? (uint32_t)KBF_CHECKED(e[u].y, a.B_rows) : kNoRecord,
+                            col_bytes, xb[u]);
+        } else if constexpr (BUF) {
           load_row_buffer<VEC>(arsrc,
                                (triple || res_row)
                                    ? (uint32_t)KBF_CHECKED(ia, a.A_rows) * row_bytes + col_bytes
@@ -428,7 +483,8 @@ stream_kernel(StreamArgs a) {
           acc[v] = __builtin_fma(t, (double)held_b[v], acc[v]);
         }
         const int f = e[u].y;
-        if (!triple && active && f != INT_MIN) {
+        if (!triple) {
+        if (active && f != INT_MIN) {
           double y[VEC];
 #pragma unroll
           for (int v = 0; v < VEC; ++v)
@@ -450,8 +506,11 @@ stream_kernel(StreamArgs a) {
               store_slot<VEC>(a.slots + (size_t)KBF_CHECKED(-(f + 1), a.n_slots) * bb + c, y);
           }
         }
+        // The marker ends the row: restart the sum (only the lanes of
+        // groups at a marker execute this).
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) acc[v] = triple ? acc[v] : 0.0;
+        for (int v = 0; v < VEC; ++v) acc[v] = 0.0;
+        }
       }
     }
   }
@@ -745,10 +804,12 @@ struct StreamChoice {
 hipError_t choose_stream(const StreamArgs &a, const StreamOptions &o, StreamChoice *c) {
   const ColumnTiling t = column_tiling(a.b);
   if (a.chunk % kChunkQuantum != 0 || a.n % a.chunk != 0) return hipErrorInvalidValue;
-  // Raw-buffer offsets are 32-bit: tables of 4 GB or more take plain loads.
+  // Raw-buffer offsets are 32-bit and a structured buffer's record stride is
+  // at most kMaxStride bytes: tables of 4 GB or more, or rows of more than
+  // 4095 floats, take plain loads.
   const uint64_t row_bytes = (uint64_t)a.b * sizeof(float);
   const uint64_t lim = kOutOfRange;
-  const bool buf = !o.plain_loads && (!a.residual || a.Z == a.A) &&
+  const bool buf = !o.plain_loads && (!a.residual || a.Z == a.A) && row_bytes <= kMaxStride &&
                    (uint64_t)a.A_rows * row_bytes <= lim &&
                    (uint64_t)a.B_rows * row_bytes <= lim && (uint64_t)a.out_rows * row_bytes <= lim &&
                    (uint64_t)a.n_slots * (uint64_t)a.b * sizeof(double) <= lim;

@@ -148,3 +148,16 @@ def test_overlap_backward_rule(bench, monkeypatch):
     assert not bench._overlap(50_000_000, 32)
     monkeypatch.setenv("KBFOLLOW_OVERLAP_BACKWARD", "1")
     assert bench._overlap(5000, 256)
+
+
+def test_timed_phases_leave_concurrent_dx_launches_alone(bench):
+    """With the concurrent backward, a kernel that runs both the forward and
+    dX is timed on its forward launches; dR alone, or any kernel when the
+    passes run one after another, is timed on every launch."""
+    both = ["fwd_stream", "dx_stream"]
+    assert bench.timed_phases(both, True) == ["fwd_stream"]
+    assert bench.timed_phases(both, False) == both
+    assert bench.timed_phases(["dr_stream"], True) == ["dr_stream"]
+    assert bench.timed_phases(["dx_stream"], True) == ["dx_stream"]
+    assert bench.timed_phases(["fwd_stream", "dx_stream", "dr_stream"], True) == \
+        ["fwd_stream", "dr_stream"]
