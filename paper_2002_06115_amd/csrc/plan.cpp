@@ -17,6 +17,7 @@
 #include <cstdlib>
 #include <cstdio>
 #include <exception>
+#include <functional>
 #include <thread>
 
 namespace kbf {
@@ -350,24 +351,38 @@ static std::vector<uint8_t> id_classes(const LayoutHost &L, int64_t n_ids, int X
   for (int32_t a : L.col_a) ++cnt[a];
   std::vector<uint8_t> cls(n_ids);
   const int64_t k_heavy = std::min<int64_t>(n_ids, 65536);
-  std::vector<int32_t> heavy(n_ids);
-  for (int64_t i = 0; i < n_ids; ++i) heavy[i] = (int32_t)i;
-  auto heavier = [&](int32_t x, int32_t y) { return cnt[x] != cnt[y] ? cnt[x] > cnt[y] : x < y; };
-  std::partial_sort(heavy.begin(), heavy.begin() + k_heavy, heavy.end(), heavier);
+  // The k_heavy heaviest ids (ties to the smaller id), heaviest first: the
+  // count of the k-th one from a selection, then the ids above it and as
+  // many of those at it as are needed, in id order.
+  std::vector<int32_t> heavy;
+  if (k_heavy > 0) {
+    std::vector<int32_t> c(cnt);
+    std::nth_element(c.begin(), c.begin() + (k_heavy - 1), c.end(), std::greater<int32_t>());
+    const int32_t kth = c[k_heavy - 1];
+    std::vector<int32_t>().swap(c);
+    int64_t above = 0;
+    for (int64_t i = 0; i < n_ids; ++i) above += cnt[i] > kth;
+    int64_t at_kth = k_heavy - above;
+    heavy.reserve(k_heavy);
+    for (int64_t i = 0; i < n_ids; ++i)
+      if (cnt[i] > kth || (cnt[i] == kth && at_kth-- > 0)) heavy.push_back((int32_t)i);
+    std::sort(heavy.begin(), heavy.end(),
+              [&](int32_t x, int32_t y) { return cnt[x] != cnt[y] ? cnt[x] > cnt[y] : x < y; });
+  }
   std::vector<char> is_heavy(n_ids, 0);
-  for (int64_t i = 0; i < k_heavy; ++i) is_heavy[heavy[i]] = 1;
+  for (int32_t h : heavy) is_heavy[h] = 1;
   int64_t load[kMaxXcd] = {};
   for (int64_t i = 0; i < n_ids; ++i)
     if (!is_heavy[i]) {
       cls[i] = (uint8_t)(i % X);
       load[i % X] += cnt[i];
     }
-  for (int64_t i = 0; i < k_heavy; ++i) {
+  for (int32_t h : heavy) {
     int best = 0;
     for (int k = 1; k < X; ++k)
       if (load[k] < load[best]) best = k;
-    cls[heavy[i]] = (uint8_t)best;
-    load[best] += cnt[heavy[i]];
+    cls[h] = (uint8_t)best;
+    load[best] += cnt[h];
   }
   return cls;
 }
@@ -429,6 +444,9 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
   } else {
     int64_t load[kMaxXcd] = {};
     std::vector<uint64_t> key;
+    std::vector<int32_t> idx;
+    std::vector<std::pair<uint64_t, int32_t>> kp;
+    const int sort_threads = std::max(1, host_threads() / 3);
     std::vector<const RowSpan *> small;
     int64_t total = 0;
     for (const RowSpan &r : rows) {
@@ -439,20 +457,38 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
         continue;
       }
       // (class, gathered id, second operand) or (class, second operand,
-      // gathered id), both below 2^30: one 64-bit key per triple.
-      key.resize(len);
-      for (int64_t i = 0; i < len; ++i) {
-        const int64_t l = r.beg + i;
+      // gathered id) as one 64-bit key per triple, the ids in as many bits
+      // as the row's largest needs (at most 3 + 30 + 30), sorted stably:
+      // long rows by the radix sort, others as (key, position) pairs.
+      uint64_t mx = 0, my = 0;
+      for (int64_t l = r.beg; l < r.end; ++l) {
+        mx = std::max<uint64_t>(mx, (uint64_t)(opt.hub_by_a ? L.col_a[l] : L.col_b[l]));
+        my = std::max<uint64_t>(my, (uint64_t)(opt.hub_by_a ? L.col_b[l] : L.col_a[l]));
+      }
+      int bx = 0, by = 0;
+      while (bx < 63 && (mx >> bx) != 0) ++bx;
+      while (by < 63 && (my >> by) != 0) ++by;
+      auto key_of = [&](int64_t l) {
         const uint64_t c = (uint64_t)cls_of(L.col_a[l]);
         const uint64_t x = (uint64_t)(opt.hub_by_a ? L.col_a[l] : L.col_b[l]);
         const uint64_t y = (uint64_t)(opt.hub_by_a ? L.col_b[l] : L.col_a[l]);
-        key[i] = (c << 60) | (x << 30) | y;
+        return (c << (bx + by)) | (x << by) | y;
+      };
+      if (len >= (int64_t(1) << 16)) {
+        key.resize(len);
+        idx.resize(len);
+        for (int64_t i = 0; i < len; ++i) {
+          key[i] = key_of(r.beg + i);
+          idx[i] = (int32_t)i;
+        }
+        radix_sort(key, &idx, sort_threads);
+        for (int64_t i = 0; i < len; ++i) pos[r.beg + i] = (int32_t)(r.beg + idx[i]);
+      } else {
+        kp.resize(len);
+        for (int64_t i = 0; i < len; ++i) kp[i] = {key_of(r.beg + i), (int32_t)i};
+        std::sort(kp.begin(), kp.end());
+        for (int64_t i = 0; i < len; ++i) pos[r.beg + i] = (int32_t)(r.beg + kp[i].second);
       }
-      std::vector<int32_t> idx(len);
-      for (int64_t i = 0; i < len; ++i) idx[i] = (int32_t)i;
-      std::stable_sort(idx.begin(), idx.end(),
-                       [&](int32_t u, int32_t v) { return key[u] < key[v]; });
-      for (int64_t i = 0; i < len; ++i) pos[r.beg + i] = (int32_t)(r.beg + idx[i]);
       // One segment per class present.
       std::vector<Seg> mine;
       for (int64_t b0 = r.beg, b1; b0 < r.end; b0 = b1) {
@@ -582,6 +618,12 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
   // Chunk order inside each list: hub chunks by their first gathered id,
   // then the others in stream order.
   P.xcd_chunk.assign(1, 0);
+  {
+    size_t total_entries = 0;
+    for (int x = 0; x < X; ++x) total_entries += S[x].size();
+    P.entries.reserve(total_entries);
+    if (weighted) P.weights.reserve(total_entries);
+  }
   for (int x = 0; x < X; ++x) {
     const int64_t nc = (int64_t)S[x].size() / chunk;
     std::vector<int64_t> co(nc);

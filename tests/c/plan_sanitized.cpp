@@ -258,6 +258,15 @@ int main() {
     }
     run_case("hub", 10, 2, s, r, o, true);
   }
+  // Rows of 2^16 triples or more: their class segments are ordered by the
+  // radix sort (shorter hub rows by a sort of key / position pairs).
+  {
+    const int64_t n_t = 70000;
+    std::uniform_int_distribution<int32_t> E(0, 4999);
+    std::vector<int32_t> s(n_t, 3), r(n_t, 0), o(n_t);
+    for (int64_t l = 0; l < n_t; ++l) o[l] = l % 2 ? E(g) : (int32_t)(l % 11);
+    run_case("long hub", 5000, 1, s, r, o, false);
+  }
   // Sparse id space: few triples over many ids (the comparison-sort path).
   {
     const int64_t n_e = 1 << 20, n_t = 3000;
