@@ -204,7 +204,7 @@ static std::vector<int32_t> offsets_of(const std::vector<int32_t> &row, int64_t 
 }
 
 // Host threads the layout build may use: the hardware's count, at most 16
-// (a GPU machine's CPU share), or KBFOLLOW_HOST_THREADS when set (>= 1).
+// (one GPU's share of a host), or KBFOLLOW_HOST_THREADS when set (>= 1).
 static int host_threads() {
   if (const char *v = std::getenv("KBFOLLOW_HOST_THREADS")) {
     const int n = std::atoi(v);
