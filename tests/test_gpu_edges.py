@@ -46,8 +46,11 @@ def rand_io(seed, b, n_e, n_r):
             g.standard_normal((b, n_e)).astype(np.float32))
 
 
-@pytest.mark.parametrize("b", [1, 2, 3, 4, 5, 8, 12, 33, 64, 100, 260, 300, 513])
+@pytest.mark.parametrize("b", [1, 2, 3, 4, 5, 8, 12, 33, 64, 100, 260, 300, 513, 4095, 4096])
 def test_batch_sizes(kbf, b):
+    # Rows are gathered as records of a structured buffer whose stride is the
+    # row's bytes, at most 16383: b = 4095 is the widest row read that way,
+    # b = 4096 takes plain loads.
     n_e, n_r = 700, 6
     s, r, o = rand_kb(b, n_e, n_r, 6000)
     X, R, dY = rand_io(b, b, n_e, n_r)
