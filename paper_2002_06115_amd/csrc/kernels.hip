@@ -42,6 +42,20 @@
 #include <mutex>
 #include <utility>
 
+// Structured-buffer loads (LLVM's amdgcn struct buffer load intrinsics): the
+// bytes at `off` of record `idx` of a descriptor whose records are `stride`
+// bytes apart.  A record index at or past the descriptor's record count
+// returns zeros without a memory access, so a gathered row needs no multiply
+// for its address and a marker's index (bit 31 set) needs no select.  (At
+// file scope: an intrinsic declared by its assembler name needs external
+// linkage.)
+typedef float kbf_float4 __attribute__((ext_vector_type(4)));
+__device__ kbf_float4 struct_buffer_load_f32x4(__amdgpu_buffer_rsrc_t rsrc, int idx, int off,
+                                               int soff, int aux)
+    __asm("llvm.amdgcn.struct.ptr.buffer.load.v4f32");
+__device__ float struct_buffer_load_f32(__amdgpu_buffer_rsrc_t rsrc, int idx, int off, int soff,
+                                        int aux) __asm("llvm.amdgcn.struct.ptr.buffer.load.f32");
+
 namespace kbf {
 
 namespace {
@@ -60,6 +74,7 @@ constexpr int kUnroll = 8;    // entries per step; a lane group keeps their load
 constexpr int kFillPieces = 4;
 constexpr int kFillBatch = 4;
 static_assert(kChunkQuantum % kUnroll == 0, "a chunk is a whole number of steps");
+static_assert(kUnroll == kStepEntries, "the planner's kSameA flags assume this step length");
 
 // Buffer-resource word 3 for gfx9-family buffers, and an offset past any raw
 // buffer this library makes (such a load returns zeros without touching
@@ -124,17 +139,6 @@ __device__ __forceinline__ void load_row(const float *__restrict__ p, float (&v)
 }
 
 typedef float native_float4 __attribute__((ext_vector_type(4)));
-
-// Structured-buffer loads (LLVM's amdgcn struct buffer load intrinsics): the
-// bytes at `off` of record `idx` of a descriptor whose records are `stride`
-// bytes apart.  A record index at or past the descriptor's record count
-// returns zeros without a memory access, so a gathered row needs no multiply
-// for its address and a marker's index (bit 31 set) needs no select.
-__device__ native_float4 struct_buffer_load_f32x4(__amdgpu_buffer_rsrc_t rsrc, int idx, int off,
-                                                  int soff, int aux)
-    __asm("llvm.amdgcn.struct.ptr.buffer.load.v4f32");
-__device__ float struct_buffer_load_f32(__amdgpu_buffer_rsrc_t rsrc, int idx, int off, int soff,
-                                        int aux) __asm("llvm.amdgcn.struct.ptr.buffer.load.f32");
 
 // Record index that no table of this library reaches.
 constexpr uint32_t kNoRecord = 0xFFFFFFFFu;
@@ -416,6 +420,12 @@ stream_kernel(StreamArgs a) {
       for (int u = 0; u < kUnroll; ++u) {
         const bool triple = e[u].x >= 0;
         const bool run_start = triple && (e[u].x & kRunStart);
+        // The entry before it in this step gathered the same A row: no read
+        // (the FMAs below take that row again).  Never at a step's first
+        // entry; the residual variants read the row again (the reuse cost
+        // their register-capped LDS form more spills than it saved).
+        const bool same_a = !RES && u > 0 && triple && (e[u].y & kSameA);
+        const int32_t bid = e[u].y & kIdMask;  // a triple's B row
         // A marker that writes row j of a residual pass reads A[j] for gamma * A[j].
         const bool res_row = RES && !triple && e[u].y >= 0;
         const uint32_t ia = triple ? (uint32_t)(e[u].x & kIdMask) : (uint32_t)e[u].y;
@@ -423,23 +433,24 @@ stream_kernel(StreamArgs a) {
           // A triple's record is its id; a marker's x (-1) with the run-start
           // bit cleared is past every table, so it reads zeros.
 #if defined(KBFOLLOW_CHECKED)
-          const uint32_t ra = triple ? (uint32_t)KBF_CHECKED(ia, a.A_rows) : kNoRecord;
+          const uint32_t ra =
+              (triple && !same_a) ? (uint32_t)KBF_CHECKED(ia, a.A_rows) : kNoRecord;
 #else
-          const uint32_t ra = (uint32_t)e[u].x & ~(uint32_t)kRunStart;
+          const uint32_t ra = same_a ? kNoRecord : ((uint32_t)e[u].x & ~(uint32_t)kRunStart);
 #endif
           gather_row<VEC>(arsrc, ra, col_bytes, xa[u]);
           if constexpr (!LDSB)
-            gather_row<VEC>(brsrc, run_start ? (uint32_t)KBF_CHECKED(e[u].y, a.B_rows) : kNoRecord,
+            gather_row<VEC>(brsrc, run_start ? (uint32_t)KBF_CHECKED(bid, a.B_rows) : kNoRecord,
                             col_bytes, xb[u]);
         } else if constexpr (BUF) {
           load_row_buffer<VEC>(arsrc,
-                               (triple || res_row)
+                               ((triple && !same_a) || res_row)
                                    ? (uint32_t)KBF_CHECKED(ia, a.A_rows) * row_bytes + col_bytes
                                    : kOutOfRange,
                                xa[u]);
           if constexpr (!LDSB)
             load_row_buffer<VEC>(brsrc,
-                                 run_start ? (uint32_t)KBF_CHECKED(e[u].y, a.B_rows) * row_bytes +
+                                 run_start ? (uint32_t)KBF_CHECKED(bid, a.B_rows) * row_bytes +
                                                  col_bytes
                                            : kOutOfRange,
                                  xb[u]);
@@ -451,7 +462,7 @@ stream_kernel(StreamArgs a) {
                                   bb +
                               cl,
                         xa[u]);
-          load_row<VEC>(a.B + (size_t)(run_start ? KBF_CHECKED(e[u].y, a.B_rows) : 0) * bb + cl,
+          load_row<VEC>(a.B + (size_t)(run_start ? KBF_CHECKED(bid, a.B_rows) : 0) * bb + cl,
                         xb[u]);
         }
       }
@@ -460,11 +471,21 @@ stream_kernel(StreamArgs a) {
       for (int u = 0; u < kUnroll; ++u) {
         const bool triple = e[u].x >= 0;
         const bool run_start = triple && (e[u].x & kRunStart);
+        // A repeated A row was not read again: take the previous entry's
+        // (plain loads read it again, the same values).
+        if constexpr (BUF && !RES) {
+          if (u > 0) {
+            const bool same_a = triple && (e[u].y & kSameA);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) xa[u][v] = same_a ? xa[u - 1][v] : xa[u][v];
+          }
+        }
         // Run starts take the new B row; markers take the zeros their
         // out-of-range B load returned (masked explicitly without BUF).
         if constexpr (LDSB) {
           if (run_start) {
-            lds_row<VEC>(b_lds + (size_t)KBF_CHECKED(e[u].y, a.B_rows) * W + lane * VEC, held_b);
+            lds_row<VEC>(b_lds + (size_t)KBF_CHECKED(e[u].y & kIdMask, a.B_rows) * W + lane * VEC,
+                         held_b);
           } else if (!triple) {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) held_b[v] = 0.0f;

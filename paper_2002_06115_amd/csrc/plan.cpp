@@ -548,7 +548,7 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
     for (const Seg &g : segs[x]) {
       int32_t parts = 0;
       bool pending = false;  // triples of this segment since the last marker
-      int32_t prev_b = 0;
+      int32_t prev_b = 0, prev_a = -1;
       for (int64_t p = g.beg; p < g.end; ++p) {
         if ((int64_t)E.size() % chunk == chunk - 1) {
           // The chunk's last entry must be a marker.
@@ -561,6 +561,10 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
         const int32_t l = pos[p];
         // A run starts after every marker and wherever col_b changes.
         const bool run_start = !pending || L.col_b[l] != prev_b;
+        // The previous entry (a triple of this row, not across a step
+        // boundary) gathered the same row: the kernel reuses it.
+        const bool same_a = pending && L.col_a[l] == prev_a &&
+                            (int64_t)E.size() % kStepEntries != 0;
         const int64_t c = (int64_t)E.size() / chunk;
         if ((int64_t)first_a[x].size() <= c) {
           first_a[x].resize(c + 1, -1);
@@ -570,9 +574,10 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
           first_a[x][c] = L.col_a[l];
           hub_chunk[x][c] = g.hub;
         }
-        E.push_back({L.col_a[l] | (run_start ? kRunStart : 0), L.col_b[l]});
+        E.push_back({L.col_a[l] | (run_start ? kRunStart : 0), L.col_b[l] | (same_a ? kSameA : 0)});
         if (weighted) Wv.push_back(L.weight[l]);
         prev_b = L.col_b[l];
+        prev_a = L.col_a[l];
         pending = true;
       }
       if (!g.alone || parts > 0)

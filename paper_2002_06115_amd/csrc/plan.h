@@ -38,16 +38,23 @@ struct LayoutHost {
 
 // One 8-byte stream entry.  A triple: x = (id gathered for this triple, col_a)
 // | kRunStart when it is the first triple of a run of equal col_b since the
-// last marker, y = col_b.  A marker (x = kMarker): write the running sum to y
-// -- a row (y >= 0), a workspace slot -(y + 1), or nothing (y = kNoTarget) --
-// and restart from zero.
+// last marker, y = col_b | kSameA when the entry right before it is a triple
+// of the same row with the same col_a and both lie in one kernel step of
+// kStepEntries entries (the kernel then reuses that entry's gathered row
+// instead of reading it again).  A marker (x = kMarker): write the running
+// sum to y -- a row (y >= 0), a workspace slot -(y + 1), or nothing
+// (y = kNoTarget) -- and restart from zero.
 struct Entry {
   int32_t x, y;
 };
 constexpr int32_t kMarker = -1;
 constexpr int32_t kRunStart = 1 << 30;
+constexpr int32_t kSameA = 1 << 30;
 constexpr int32_t kIdMask = kRunStart - 1;
 constexpr int32_t kNoTarget = INT32_MIN;
+// Entries a lane group takes per kernel step (the stream kernel's unroll):
+// chunks start at multiples of it, so steps are aligned in the stream.
+constexpr int32_t kStepEntries = 8;
 
 // The stream plan of one layout.  The sorted triples of every non-empty row
 // are followed by a marker that writes the row, and the stream is cut into

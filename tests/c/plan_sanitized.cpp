@@ -111,18 +111,30 @@ static void interpret_plan(const LayoutHost &L, const PlanHost &P, int32_t chunk
     int64_t acc = 0;
     bool held = false;
     int32_t hb = 0;
+    int32_t held_a = -1;  // the A row the previous entry gathered (or reused)
     for (int64_t p = c * chunk; p < (c + 1) * chunk; ++p) {
       const Entry &e = P.entries[p];
       if (e.x >= 0) {
-        const int32_t a = e.x & kIdMask;
+        const int32_t b = e.y & kIdMask;
+        int32_t a = e.x & kIdMask;
+        if (e.y & kSameA) {
+          // The kernel skips this gather and takes the previous entry's row:
+          // only inside a step, after a triple with the same id.
+          CHECK(p % kStepEntries != 0 && held_a == a,
+                "%s: entry %lld reuses a row it may not (step start or other id)", what,
+                (long long)p);
+          a = held_a;
+        }
         if (e.x & kRunStart) {
-          hb = e.y;
+          hb = b;
           held = true;
         }
-        CHECK(held && hb == e.y, "%s: entry %lld outside a run of its second operand", what,
+        CHECK(held && hb == b, "%s: entry %lld outside a run of its second operand", what,
               (long long)p);
-        acc += val(a, e.y);
+        acc += val(a, b);
+        held_a = a;
       } else {
+        held_a = -1;
         if (e.y >= 0 && e.y < L.rows) {
           got[e.y] += acc;
           ++writes[e.y];
