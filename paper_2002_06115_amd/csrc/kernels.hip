@@ -273,15 +273,19 @@ __device__ __forceinline__ void store_row_buffer(__amdgpu_buffer_rsrc_t rsrc, ui
 // and adds w * A[a] * B[b_id] for every triple with one double FMA per
 // column (the product of two floats is exact in double).
 //
-// With BUF (A, B, the output and the workspace each under 4 GB) all reads are
-// raw buffer loads with 32-bit offsets; where no row is needed (A at markers,
-// B except at run starts) the offset is out of range, so the lane gets zeros
-// and generates no memory traffic, and no load sits behind a branch.  A
-// marker therefore finds A = 0 and a held B row of 0, so its FMA adds an
-// exact zero.  Without BUF, plain loads read row 0 at markers and the values
-// are masked instead.
+// With BUF (A, B, the output and the workspace each under 4 GB, rows of at
+// most kMaxStride bytes) all reads are buffer loads: A and B rows through
+// structured buffers (record = row id), the residual variants' rows and the
+// stores through raw 32-bit byte offsets.  Where no row is needed (A at
+// markers and where the step's previous entry gathered the same row, B
+// except at run starts) the record or offset is out of range, so the lane
+// gets zeros and generates no memory traffic, and no load sits behind a
+// branch.  A marker therefore finds A = 0 and a held B row of 0, so its FMA
+// adds an exact zero; a repeated row takes the previous entry's values.
+// Without BUF, plain loads read row 0 at markers and the values are masked
+// instead.
 //
-// With LDSB (raw buffer loads only) the workgroup first copies its column
+// With LDSB (buffer loads only) the workgroup first copies its column
 // slice of the whole B table into LDS, and a run start reads its B row from
 // there when the FMAs need it.  No B row is then held in registers while a
 // step's gathers are in flight, which leaves room for more waves per SIMD,
