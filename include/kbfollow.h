@@ -110,7 +110,21 @@ typedef enum {
  *                                       on small KBs; bitwise the same);
  *   KBFOLLOW_HOST_THREADS               host threads for the layout sorts
  *                                       (default: the hardware's, at most 16;
- *                                       the same layouts for any count).
+ *                                       the same layouts for any count);
+ *   KBFOLLOW_XCD                        chunk lists, one per XCD (8; 1 keeps
+ *                                       one list in row order);
+ *   KBFOLLOW_HUB_MIN                    triples from which a row is split
+ *                                       into one segment per class of its
+ *                                       gathered ids (256);
+ *   KBFOLLOW_BAND=0                     hub chunks in stream order instead of
+ *                                       by first gathered id;
+ *   KBFOLLOW_MAX_LPT                    widest lane group of the register
+ *                                       variant, every pass (default: 32, 8
+ *                                       for dR from b = 128; bitwise the
+ *                                       same);
+ *   KBFOLLOW_STREAM_STAMPS=0            phase timing of the stream kernels by
+ *                                       event records instead of their
+ *                                       dispatch timestamps.
  */
 kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
                     const int32_t *subj, const int32_t *rel, const int32_t *obj,
