@@ -292,22 +292,35 @@ def phase_groups(kernels, phases_ms):
     return groups
 
 
-def dominant_kernel(kernels, phases):
+def dominant_kernel(kernels, phases, concurrent=False):
     """(kernel, its phases, {kernel: ms per step}, why): the kernel with the
     largest share of the step's GPU time (sum of its launches' durations).
     Where that is not a stream kernel (small KBs, whose combine and empty-row
     launches take longer than their stream kernels) the stream kernel with the
-    largest share is taken, since only the stream kernels have a byte model."""
+    largest share is taken, since only the stream kernels have a byte model.
+    With the concurrent backward, the dX and dR launches overlap and each one's
+    duration includes the time it shares the GPU with the other; where the
+    two largest shares are within 5 % of each other, the kernel that also runs
+    a launch of its own (the forward) is taken, whose duration is its own."""
     groups = phase_groups(kernels, phases)
     share = {k: sum(phases[p][0] for p in ps) for k, ps in groups.items()}
+    streams = [k for k, ps in groups.items() if all(p.endswith("_stream") for p in ps)]
     top = max(share, key=share.get)
     why = "largest share of the step's GPU time (sum of launch durations)"
-    if not all(p.endswith("_stream") for p in groups[top]):
-        streams = [k for k, ps in groups.items() if all(p.endswith("_stream") for p in ps)]
+    if top not in streams:
         top2 = max(streams, key=share.get)
         why = (f"the stream kernel with the largest share of the step's GPU time ({top}, a "
                f"combine / empty-row kernel, has more)")
         top = top2
+    if concurrent:
+        overlapped = lambda k: all(p.startswith(("dx_", "dr_")) for p in groups[k])
+        rivals = [k for k in streams if k != top and share[k] >= 0.95 * share[top]
+                  and not overlapped(k)]
+        if overlapped(top) and rivals:
+            top = max(rivals, key=share.get)
+            why = ("within 5 % of the largest share of the step's GPU time, the stream kernel "
+                   "with launches outside the concurrent backward (the largest share belongs "
+                   "to a kernel whose launches all overlap another pass)")
     return top, groups[top], share, why
 
 
@@ -330,7 +343,7 @@ def roofline_entry(kb, w, b, kernels, phases, timed, ms_step, residual, concurre
     algorithmic bytes of its launches (array-once model: each gathered array
     read once, every output row the kernel writes) / their duration, over the
     launches the timed steps bracketed (timed_phases)."""
-    dom, dom_phases, share, choice = dominant_kernel(kernels, phases)
+    dom, dom_phases, share, choice = dominant_kernel(kernels, phases, concurrent)
     total = sum(share.values()) or 1.0
     t_phases = timed_phases(dom_phases, concurrent)
     ms_sum = sum(timed[p][0] for p in t_phases)
@@ -356,6 +369,19 @@ def roofline_entry(kb, w, b, kernels, phases, timed, ms_step, residual, concurre
             "distinct_rows_frac": round(per_launch["distinct"] / sec / 1e9 / PEAK_HBM_GBPS, 4),
             "gather_model_bytes": per_launch["gather"],
             "gather_model_GBps": round(per_launch["gather"] / sec / 1e9, 1)}
+    # The other stream kernels, from the phase loop (every phase bracketed).
+    others = []
+    for k, ps in phase_groups(kernels, phases).items():
+        if k == dom or not all(p.endswith("_stream") for p in ps):
+            continue
+        ms_k = sum(phases[p][0] for p in ps) / max(1, sum(phases[p][1] for p in ps))
+        by_k = float(np.mean([pass_bytes(kb, b, p.split("_")[0])["array_once"] for p in ps]))
+        others.append({"kernel": k, "phases": ps, "gpu_time_share": round(share[k] / total, 4),
+                       "kernel_ms_phase_loop": round(ms_k, 4),
+                       "frac": round(by_k / (ms_k * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                       "overlaps_another_pass": concurrent and all(
+                           p.startswith(("dx_", "dr_")) for p in ps)})
+    roof["other_stream_kernels"] = others
     if traffic:
         roof["fabric_traffic_GBps"] = round(traffic / sec / 1e9, 1)
         roof["fabric_traffic_frac_upper_bound"] = round(traffic / sec / 1e9 / PEAK_HBM_GBPS, 4)
@@ -464,7 +490,7 @@ def follow_bench(args, torch, kbgen, kbf):
         raw = gkb.profile_read()
         gkb.profile(False)
         phases = {k: (v[0] / args.steps, v[1] / args.steps) for k, v in raw.items()}
-        dom_phases = dominant_kernel(kernels, phases)[1]
+        dom_phases = dominant_kernel(kernels, phases, _overlap(kb.n_triples, b))[1]
         gkb.profile(True, phases=timed_phases(dom_phases, _overlap(kb.n_triples, b)))
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)

@@ -448,6 +448,12 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
       const int32_t n_xcd = std::max(1, std::min(kMaxXcd, env_int("KBFOLLOW_XCD", 8)));
       const int64_t hub_min = std::max(1, env_int("KBFOLLOW_HUB_MIN", 256));
       const bool band = env_int("KBFOLLOW_BAND", 1) != 0;
+      // The dR lists are split by the class of the subject (the X row read
+      // once per run), not of the gathered object: every (relation, subject)
+      // run stays whole, 29 % fewer X reads on the 10 M-entity KB, and dR
+      // took 0.838 -> 0.816 ms (training-shaped KB 3.84 -> 3.71 ms) although
+      // its dY gathers no longer stay in one XCD's class.
+      const bool dr_class_b = env_int("KBFOLLOW_DR_CLASS_B", 1) != 0;
       PlanHost P[3];
       std::exception_ptr err[3];
       auto plan = [&](int k) {
@@ -460,6 +466,8 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
           po.hub_by_a = k != BY_REL;
           po.band = band;
           po.n_ids_a = n_entities;  // subjects (forward) or objects (dX, dR)
+          po.class_by_b = k == BY_REL && dr_class_b;
+          po.n_ids_b = n_entities;  // subjects (dR)
           P[k] = plan_layout(H[k], po);
           H[k] = LayoutHost{H[k].rows};  // the sorted rows are no longer needed
         } catch (...) {

@@ -344,11 +344,11 @@ static void add_empty(PlanHost &P, int64_t first, int64_t count) {
 // gather each: the heaviest ids one by one onto the lightest class, the
 // others by id modulo n_xcd.  Empty when the id space is far larger than the
 // KB (then the class of id a is a % n_xcd).
-static std::vector<uint8_t> id_classes(const LayoutHost &L, int64_t n_ids, int X) {
-  const int64_t n_t = (int64_t)L.col_a.size();
+static std::vector<uint8_t> id_classes(const std::vector<int32_t> &col, int64_t n_ids, int X) {
+  const int64_t n_t = (int64_t)col.size();
   if (X <= 1 || n_ids <= 0 || n_ids > 4 * n_t + (int64_t(1) << 20)) return {};
   std::vector<int32_t> cnt(n_ids, 0);
-  for (int32_t a : L.col_a) ++cnt[a];
+  for (int32_t a : col) ++cnt[a];
   std::vector<uint8_t> cls(n_ids);
   const int64_t k_heavy = std::min<int64_t>(n_ids, 65536);
   // The k_heavy heaviest ids (ties to the smaller id), heaviest first: the
@@ -426,9 +426,13 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
   // inside hub rows of a plan with several lists.
   std::vector<int32_t> pos(n_t);
   for (int64_t i = 0; i < n_t; ++i) pos[i] = (int32_t)i;
-  const std::vector<uint8_t> cls_tab = id_classes(L, opt.n_ids_a, X);
-  auto cls_of = [&](int32_t a) -> int {
-    return cls_tab.empty() ? (int)(a % X) : (int)cls_tab[a];
+  const std::vector<int32_t> &cls_col = opt.class_by_b ? L.col_b : L.col_a;
+  const std::vector<uint8_t> cls_tab =
+      id_classes(cls_col, opt.class_by_b ? opt.n_ids_b : opt.n_ids_a, X);
+  // The class of the triple at position l.
+  auto cls_at = [&](int64_t l) -> int {
+    const int32_t id = cls_col[l];
+    return cls_tab.empty() ? (int)(id % X) : (int)cls_tab[id];
   };
 
   // Segments per list: a hub row's class segments first (rows in order),
@@ -469,7 +473,7 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
       while (bx < 63 && (mx >> bx) != 0) ++bx;
       while (by < 63 && (my >> by) != 0) ++by;
       auto key_of = [&](int64_t l) {
-        const uint64_t c = (uint64_t)cls_of(L.col_a[l]);
+        const uint64_t c = (uint64_t)cls_at(l);
         const uint64_t x = (uint64_t)(opt.hub_by_a ? L.col_a[l] : L.col_b[l]);
         const uint64_t y = (uint64_t)(opt.hub_by_a ? L.col_b[l] : L.col_a[l]);
         return (c << (bx + by)) | (x << by) | y;
@@ -492,15 +496,15 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
       // One segment per class present.
       std::vector<Seg> mine;
       for (int64_t b0 = r.beg, b1; b0 < r.end; b0 = b1) {
-        const int c = cls_of(L.col_a[pos[b0]]);
-        for (b1 = b0 + 1; b1 < r.end && cls_of(L.col_a[pos[b1]]) == c;) ++b1;
+        const int c = cls_at(pos[b0]);
+        for (b1 = b0 + 1; b1 < r.end && cls_at(pos[b1]) == c;) ++b1;
         mine.push_back({r.row, b0, b1, false, true});
         load[c] += b1 - b0 + 1;
       }
       const bool alone = mine.size() == 1;
       for (Seg &g : mine) {
         g.alone = alone;
-        segs[cls_of(L.col_a[pos[g.beg]])].push_back(g);
+        segs[cls_at(pos[g.beg])].push_back(g);
       }
     }
     // Whole rows: the list of their first gathered id's class while it has
@@ -509,7 +513,7 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
     const int64_t target = (total + X - 1) / X;
     for (const RowSpan *r : small) {
       const int64_t w = r->end - r->beg + 1;
-      int c = cls_of(L.col_a[r->beg]);
+      int c = cls_at(r->beg);
       if (load[c] + w > target) {
         for (int k = 0; k < X; ++k)
           if (load[k] < load[c]) c = k;

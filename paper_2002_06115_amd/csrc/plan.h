@@ -78,12 +78,13 @@ constexpr int32_t kEmptyPiece = 4096;
 // Chunk lists: the stream is cut into n_xcd consecutive lists of whole
 // chunks, list x for the workgroups that run on XCD x (workgroup w runs on
 // XCD w mod 8 on an MI355X), so that each XCD's L2 caches the rows its own
-// triples gather.  The gathered ids are split into n_xcd classes of about
-// equal weight; a row with at least hub_min triples is cut into one segment
-// per class present, each in its class's list (its partial sums go to slots
-// and are combined like those of a row that crosses chunks), and every other
-// row goes whole into one list (the class of its first gathered id, unless
-// that list is already full).  Inside a hub segment the triples are ordered
+// triples gather.  The gathered ids (or, with class_by_b, the second
+// operand's) are split into n_xcd classes of about equal weight; a row with
+// at least hub_min triples is cut into one segment per class present, each
+// in its class's list (its partial sums go to slots and are combined like
+// those of a row that crosses chunks), and every other row goes whole into
+// one list (the class of its first triple, unless that list is already
+// full).  Inside a hub segment the triples are ordered
 // by gathered id (hub_by_a) or by (second operand, gathered id), and a
 // list's hub chunks are ordered by their first gathered id (band), so that
 // the chunks in flight at once gather from nearby rows.  The order of
@@ -97,6 +98,10 @@ struct PlanOptions {
   bool hub_by_a = true;
   bool band = true;
   int64_t n_ids_a = 0;     // size of the gathered id space
+  // Classes of the second operand's ids instead of the gathered ones (every
+  // run of equal second operand then stays in one list).
+  bool class_by_b = false;
+  int64_t n_ids_b = 0;     // size of the second operand's id space
 };
 
 struct PlanHost {

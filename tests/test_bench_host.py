@@ -161,3 +161,17 @@ def test_timed_phases_leave_concurrent_dx_launches_alone(bench):
     assert bench.timed_phases(["dx_stream"], True) == ["dx_stream"]
     assert bench.timed_phases(["fwd_stream", "dx_stream", "dr_stream"], True) == \
         ["fwd_stream", "dr_stream"]
+
+
+def test_dominant_kernel_near_tie_prefers_a_kernel_with_launches_of_its_own(bench):
+    """Shares within 5 %: with the concurrent backward the kernel whose
+    launches all overlap another pass gives way; otherwise the larger share
+    wins, and a clear winner keeps its place."""
+    kernels = {"fwd_stream": "K1", "dx_stream": "K1", "dr_stream": "K2",
+               "fwd_tail": "T", "dx_tail": "T", "dr_tail": "T"}
+    phases = {"fwd_stream": (0.72, 1), "dx_stream": (0.82, 1), "dr_stream": (1.56, 1),
+              "fwd_tail": (0.15, 1), "dx_tail": (0.69, 1), "dr_tail": (0.02, 1)}
+    assert bench.dominant_kernel(kernels, phases, concurrent=True)[0] == "K1"
+    assert bench.dominant_kernel(kernels, phases, concurrent=False)[0] == "K2"
+    phases["dr_stream"] = (1.80, 1)
+    assert bench.dominant_kernel(kernels, phases, concurrent=True)[0] == "K2"
