@@ -118,6 +118,9 @@ typedef enum {
  *                                       gathered ids (256);
  *   KBFOLLOW_BAND=0                     hub chunks in stream order instead of
  *                                       by first gathered id;
+ *   KBFOLLOW_DR_CLASS_B=0               dR's chunk lists classed by the
+ *                                       gathered object id instead of the
+ *                                       subject id held per run;
  *   KBFOLLOW_MAX_LPT                    widest lane group of the register
  *                                       variant, every pass (default: 32, 8
  *                                       for dR from b = 128; bitwise the
