@@ -121,6 +121,8 @@ typedef enum {
  *   KBFOLLOW_DR_CLASS_B=0               dR's chunk lists classed by the
  *                                       gathered object id instead of the
  *                                       subject id held per run;
+ *   KBFOLLOW_DR_BLOCKS                  blocks of the object id leading
+ *                                       dR's hub segments (16; 0 or 1: none);
  *   KBFOLLOW_MAX_LPT                    widest lane group of the register
  *                                       variant, every pass (default: 32, 8
  *                                       for dR from b = 128; bitwise the

@@ -443,8 +443,8 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
       // a single list in row order).  Hub rows (KBFOLLOW_HUB_MIN triples or
       // more) are split by the class of the gathered id; in the forward and
       // dX passes (second operand R, read from LDS) their triples are ordered
-      // by gathered id, in the dR pass by (subject, object), which keeps the
-      // runs of equal subject whose X row is read once.
+      // by gathered id, in the dR pass by (object block, subject, object),
+      // which keeps runs of equal subject, whose X row is read once per run.
       const int32_t n_xcd = std::max(1, std::min(kMaxXcd, env_int("KBFOLLOW_XCD", 8)));
       const int64_t hub_min = std::max(1, env_int("KBFOLLOW_HUB_MIN", 256));
       const bool band = env_int("KBFOLLOW_BAND", 1) != 0;
@@ -454,6 +454,11 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
       // took 0.838 -> 0.816 ms (training-shaped KB 3.84 -> 3.71 ms) although
       // its dY gathers no longer stay in one XCD's class.
       const bool dr_class_b = env_int("KBFOLLOW_DR_CLASS_B", 1) != 0;
+      // dR's hub segments led by 16 blocks of the object id, so that the
+      // chunks in flight at once gather dY from about one block: dR 0.815 ->
+      // 0.792 ms on the 10 M-entity KB with the passes serial (8 and 32
+      // blocks the same within 1 %), training-shaped KB step 9.23 -> 9.11 ms.
+      const int32_t dr_blocks = env_int("KBFOLLOW_DR_BLOCKS", 16);
       PlanHost P[3];
       std::exception_ptr err[3];
       auto plan = [&](int k) {
@@ -468,6 +473,7 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
           po.n_ids_a = n_entities;  // subjects (forward) or objects (dX, dR)
           po.class_by_b = k == BY_REL && dr_class_b;
           po.n_ids_b = n_entities;  // subjects (dR)
+          po.a_blocks = k == BY_REL ? dr_blocks : 0;
           P[k] = plan_layout(H[k], po);
           H[k] = LayoutHost{H[k].rows};  // the sorted rows are no longer needed
         } catch (...) {

@@ -451,6 +451,8 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
     std::vector<int32_t> idx;
     std::vector<std::pair<uint64_t, int32_t>> kp;
     const int sort_threads = std::max(1, host_threads() / 3);
+    const int32_t a_blocks =
+        opt.hub_by_a ? 0 : std::max<int32_t>(0, std::min<int32_t>(opt.a_blocks, 64));
     std::vector<const RowSpan *> small;
     int64_t total = 0;
     for (const RowSpan &r : rows) {
@@ -472,11 +474,21 @@ PlanHost plan_layout(const LayoutHost &L, const PlanOptions &opt) {
       int bx = 0, by = 0;
       while (bx < 63 && (mx >> bx) != 0) ++bx;
       while (by < 63 && (my >> by) != 0) ++by;
+      // Blocks of the gathered id ahead of the second operand (3 bits of
+      // class, at most 6 of block).
+      int bk = 0;
+      if (a_blocks > 1) {
+        while ((1 << bk) < a_blocks) ++bk;
+        if (3 + bk + bx + by > 64) bk = 0;
+      }
       auto key_of = [&](int64_t l) {
         const uint64_t c = (uint64_t)cls_at(l);
         const uint64_t x = (uint64_t)(opt.hub_by_a ? L.col_a[l] : L.col_b[l]);
         const uint64_t y = (uint64_t)(opt.hub_by_a ? L.col_b[l] : L.col_a[l]);
-        return (c << (bx + by)) | (x << by) | y;
+        const uint64_t k =
+            bk ? (uint64_t)((int64_t)L.col_a[l] * a_blocks / std::max<int64_t>(1, opt.n_ids_a))
+               : 0;
+        return (c << (bk + bx + by)) | (k << (bx + by)) | (x << by) | y;
       };
       if (len >= (int64_t(1) << 16)) {
         key.resize(len);

@@ -102,6 +102,11 @@ struct PlanOptions {
   // run of equal second operand then stays in one list).
   bool class_by_b = false;
   int64_t n_ids_b = 0;     // size of the second operand's id space
+  // With hub_by_a false: hub segments ordered by (block of the gathered id,
+  // second operand, gathered id), the gathered ids cut into a_blocks equal
+  // ranges (0 or 1: no blocks), so that with band the chunks of a list walk
+  // the gathered table one block at a time.
+  int32_t a_blocks = 0;
 };
 
 struct PlanHost {

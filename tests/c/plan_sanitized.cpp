@@ -214,25 +214,29 @@ static void run_case(const char *what, int64_t n_e, int64_t n_r, std::vector<int
         interpret_plan(L[k], P, chunk, what);
       }
       // One chunk list per XCD, hub rows split by class of the gathered id
-      // (or of the second operand).
+      // (or of the second operand), and hub segments led by blocks of the
+      // gathered id.
       for (int64_t hub_min : {int64_t(4), int64_t(64)})
         for (bool by_a : {true, false})
           for (bool band : {true, false})
-            for (bool class_b : {false, true}) {
-              PlanOptions po;
-              po.chunk = chunk;
-              po.fan_in = 3;
-              po.n_xcd = 8;
-              po.hub_min = hub_min;
-              po.hub_by_a = by_a;
-              po.band = band;
-              po.n_ids_a = n_e;
-              po.class_by_b = class_b;
-              po.n_ids_b = k == 2 ? n_e : n_r;  // dR's second operand is the subject
-              const PlanHost P = plan_layout(L[k], po);
-              check_plan(L[k], P, chunk, what);
-              interpret_plan(L[k], P, chunk, what);
-            }
+            for (bool class_b : {false, true})
+              for (int32_t blocks : {0, 5}) {
+                if (by_a && blocks) continue;  // blocks order only (second operand, id) segments
+                PlanOptions po;
+                po.a_blocks = blocks;
+                po.chunk = chunk;
+                po.fan_in = 3;
+                po.n_xcd = 8;
+                po.hub_min = hub_min;
+                po.hub_by_a = by_a;
+                po.band = band;
+                po.n_ids_a = n_e;
+                po.class_by_b = class_b;
+                po.n_ids_b = k == 2 ? n_e : n_r;  // dR's second operand is the subject
+                const PlanHost P = plan_layout(L[k], po);
+                check_plan(L[k], P, chunk, what);
+                interpret_plan(L[k], P, chunk, what);
+              }
     }
   }
 }
