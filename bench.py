@@ -591,6 +591,7 @@ def follow_bench(args, torch, kbgen, kbf):
                         "with concurrent_backward the dx_* and dr_* phases run at the same "
                         "time, so their times overlap"),
         "kb_create_s": round(create_s, 2),
+        "workspace_bytes": int(gkb.workspace_size(b)),
         "timing": detail,
         "roofline": roof,
         "cpu_baseline": cpu,

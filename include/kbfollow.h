@@ -93,8 +93,9 @@ typedef enum {
  * Environment variables read here, for tests and tuning (results are the
  * same up to the summation order of split rows, or bitwise the same):
  *   KBFOLLOW_CHUNK, KBFOLLOW_REL_CHUNK  entries per chunk of the entity and
- *                                       relation layouts (default 256, less
- *                                       for small KBs; rounded up to 8);
+ *                                       relation layouts (default 256 and
+ *                                       128, less for small KBs; rounded up
+ *                                       to 8);
  *   KBFOLLOW_FAN_IN                     partials per combine task (32);
  *   KBFOLLOW_PLAIN_LOADS=1              plain loads instead of raw buffer
  *                                       loads (bitwise the same);

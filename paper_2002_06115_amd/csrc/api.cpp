@@ -428,8 +428,12 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
     };
     const int32_t chunk_seg =
         whole_steps(env_int("KBFOLLOW_CHUNK", default_chunk(n_triples + n_entities)));
-    const int32_t chunk_rel =
-        whole_steps(env_int("KBFOLLOW_REL_CHUNK", default_chunk(n_triples + n_relations)));
+    // dR's chunks at most 128 entries: with its object blocks, the shorter
+    // chunks keep the gathers in flight at once closer together (measured on
+    // one box: 10 M-entity KB step 2.369 -> 2.340 ms, training-shaped KB
+    // 9.05 -> 9.00 ms; 64 no better), for twice the partial slots.
+    const int32_t chunk_rel = whole_steps(env_int(
+        "KBFOLLOW_REL_CHUNK", std::min<int32_t>(128, default_chunk(n_triples + n_relations))));
     const int32_t fan_in = std::max(2, env_int("KBFOLLOW_FAN_IN", 32));
     {
       LayoutHost H[3];
