@@ -119,11 +119,13 @@ typedef enum {
  *                                       gathered ids (256);
  *   KBFOLLOW_BAND=0                     hub chunks in stream order instead of
  *                                       by first gathered id;
- *   KBFOLLOW_DR_CLASS_B=0               dR's chunk lists classed by the
- *                                       gathered object id instead of the
- *                                       subject id held per run;
+ *   KBFOLLOW_DR_CLASS_B=0|1             dR's chunk lists classed by the
+ *                                       gathered object id (0) or by the
+ *                                       subject id held per run (1); default:
+ *                                       by subject when the top 1 % of
+ *                                       objects hold a quarter of the triples;
  *   KBFOLLOW_DR_BLOCKS                  blocks of the object id leading
- *                                       dR's hub segments (16; 0 or 1: none);
+ *                                       dR's hub segments (64; 0 or 1: none);
  *   KBFOLLOW_MAX_LPT                    widest lane group of the register
  *                                       variant, every pass (default: 32, 8
  *                                       for dR from b = 128; bitwise the

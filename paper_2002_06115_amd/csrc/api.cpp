@@ -452,17 +452,29 @@ kb_status kb_create(int64_t n_entities, int64_t n_relations, int64_t n_triples,
       const int32_t n_xcd = std::max(1, std::min(kMaxXcd, env_int("KBFOLLOW_XCD", 8)));
       const int64_t hub_min = std::max(1, env_int("KBFOLLOW_HUB_MIN", 256));
       const bool band = env_int("KBFOLLOW_BAND", 1) != 0;
-      // The dR lists are split by the class of the subject (the X row read
-      // once per run), not of the gathered object: every (relation, subject)
-      // run stays whole, 29 % fewer X reads on the 10 M-entity KB, and dR
-      // took 0.838 -> 0.816 ms (training-shaped KB 3.84 -> 3.71 ms) although
-      // its dY gathers no longer stay in one XCD's class.
-      const bool dr_class_b = env_int("KBFOLLOW_DR_CLASS_B", 1) != 0;
-      // dR's hub segments led by 16 blocks of the object id, so that the
-      // chunks in flight at once gather dY from about one block: dR 0.815 ->
-      // 0.792 ms on the 10 M-entity KB with the passes serial (8 and 32
-      // blocks the same within 1 %), training-shaped KB step 9.23 -> 9.11 ms.
-      const int32_t dr_blocks = env_int("KBFOLLOW_DR_BLOCKS", 16);
+      // dR's lists are classed by subject (the X row read once per run) when
+      // the objects are skewed, by the gathered object when they are not
+      // (KBFOLLOW_DR_CLASS_B=1 / 0 forces one).  Skewed objects (the top 1 %
+      // by in-degree holding at least a quarter of the triples) keep their
+      // dY rows hot in the L2s under any classing, and subject classes keep
+      // every (relation, subject) run whole: on the 10 M-entity KB (top 1 %
+      // of the Zipf objects: ~80 % of the triples) dR took 0.797 ms with
+      // object classes and 0.775 with subject classes (passes serial; 3.21
+      // against 3.11 ms at b = 128, 6.51 against 6.27 at b = 256).  With
+      // near-uniform objects only the classing keeps one XCD's dY working
+      // set small: on the training-shaped KB (uniform objects) dR took 3.04
+      // ms with object classes and 3.45 with subject classes (64 blocks
+      // each; 0.391 against 0.439 ms at b = 32).
+      const int cls_env = env_int("KBFOLLOW_DR_CLASS_B", -1);
+      const bool dr_class_b = cls_env >= 0
+                                  ? cls_env != 0
+                                  : top_id_share(H[BY_REL].col_a, n_entities, 0.01) >= 0.25;
+      // dR's hub segments led by 64 blocks of the object id, so that the
+      // chunks in flight at once gather dY from a few blocks: dR 0.815 ->
+      // 0.79 ms on the 10 M-entity KB with the passes serial (8 to 32 blocks
+      // the same within 1 %); on the training-shaped KB 3.35 -> 3.04 ms with
+      // object classes (16 -> 64 blocks).
+      const int32_t dr_blocks = env_int("KBFOLLOW_DR_BLOCKS", 64);
       PlanHost P[3];
       std::exception_ptr err[3];
       auto plan = [&](int k) {

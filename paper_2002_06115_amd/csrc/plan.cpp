@@ -14,6 +14,7 @@
 #include "plan.h"
 
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <cstdio>
 #include <exception>
@@ -385,6 +386,18 @@ static std::vector<uint8_t> id_classes(const std::vector<int32_t> &col, int64_t 
     load[best] += cnt[h];
   }
   return cls;
+}
+
+double top_id_share(const std::vector<int32_t> &col, int64_t n_ids, double frac) {
+  if (col.empty() || n_ids <= 0) return 0.0;
+  std::vector<int32_t> cnt((size_t)n_ids, 0);
+  for (int32_t id : col) ++cnt[(size_t)id];
+  const int64_t k = std::min<int64_t>(
+      n_ids, std::max<int64_t>(1, (int64_t)std::ceil(frac * (double)n_ids)));
+  if (k < n_ids) std::nth_element(cnt.begin(), cnt.begin() + k, cnt.end(), std::greater<int32_t>());
+  int64_t top = 0;
+  for (int64_t i = 0; i < k; ++i) top += cnt[(size_t)i];
+  return (double)top / (double)col.size();
 }
 
 PlanHost plan_layout(const LayoutHost &L, int32_t chunk, int32_t fan_in) {

@@ -125,6 +125,10 @@ struct PlanHost {
   int64_t max_row_len = 0;
 };
 
+// The share of the entries of `col` (ids below n_ids) whose id is one of the
+// ceil(frac * n_ids) most frequent ones: how skewed the id distribution is.
+double top_id_share(const std::vector<int32_t> &col, int64_t n_ids, double frac);
+
 // Returns "" when the triple arrays are valid, else a message; *range_error
 // tells an out-of-range id (KB_ERANGE) from any other problem (KB_EINVAL).
 std::string validate_triples(int64_t n_entities, int64_t n_relations, int64_t n_triples,

@@ -256,6 +256,15 @@ int main() {
     CHECK(!validate_triples((1 << 30) + 1, 1, 0, nullptr, nullptr, nullptr, &range).empty(),
           "N_E above 2^30 accepted");
   }
+  // The skew statistic that picks dR's classing.
+  {
+    const std::vector<int32_t> col = {0, 0, 0, 1, 2, 3, 3, 0};
+    CHECK(top_id_share(col, 4, 0.25) == 0.5, "top 1 of 4 ids: half the entries");
+    CHECK(top_id_share(col, 4, 0.5) == 6.0 / 8.0, "top 2 of 4 ids: six of eight entries");
+    CHECK(top_id_share(col, 4, 1.0) == 1.0, "every id: every entry");
+    CHECK(top_id_share(col, 100, 0.01) == 0.5, "top 1 of 100 ids (one rounded up)");
+    CHECK(top_id_share({}, 4, 0.5) == 0.0, "no entries");
+  }
   // Random KBs.
   for (int rep = 0; rep < 4; ++rep) {
     const int64_t n_e = 50 + rep * 300, n_r = 1 + rep * 3, n_t = 2000 + rep * 5000;
