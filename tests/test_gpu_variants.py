@@ -72,3 +72,38 @@ def test_variant(kbf, b, weighted, gamma, path, monkeypatch):
     assert_close(from_em(dX), wantdX, label + " dX")
     assert_close(from_em(dR), wantdR, label + " dR")
     kb.close()
+
+
+@pytest.mark.parametrize("class_b,blocks,objects", itertools.product(
+    ["0", "1", None], ["0", "5", "64"], ["hubs", "uniform"]))
+def test_dr_layout_choices(kbf, class_b, blocks, objects, monkeypatch):
+    """dR's chunk lists classed by object or by subject (forced, or picked by
+    the object skew when None), its hub segments led by 0, 5 or 64 blocks of
+    the object id: every choice is a reordering of the same sums, checked
+    against the oracle on a KB with hub objects and on one with uniform
+    objects (the two sides of the skew rule)."""
+    if class_b is not None:
+        monkeypatch.setenv("KBFOLLOW_DR_CLASS_B", class_b)
+    monkeypatch.setenv("KBFOLLOW_DR_BLOCKS", blocks)
+    monkeypatch.setenv("KBFOLLOW_REL_CHUNK", "16")
+    monkeypatch.setenv("KBFOLLOW_HUB_MIN", "32")
+    if objects == "hubs":
+        s, r, o, n_e, n_r = small_kb(91)
+    else:
+        g = np.random.default_rng(92)
+        n_e, n_r, n_t = 400, 5, 8000
+        s = g.integers(0, n_e, n_t).astype(np.int32)
+        r = g.integers(0, n_r, n_t).astype(np.int32)
+        o = g.integers(0, n_e, n_t).astype(np.int32)
+    g = np.random.default_rng(93)
+    b = 32
+    X = g.standard_normal((b, n_e)).astype(np.float32)
+    R = g.standard_normal((b, n_r)).astype(np.float32)
+    dY = g.standard_normal((b, n_e)).astype(np.float32)
+    kb = kbf.KB(s, r, o, n_e, n_r)
+    dX, dR = kb.follow_backward(to_em(X), to_em(R), to_em(dY))
+    wantdX, wantdR = oracle.follow_backward(s, r, o, n_e, n_r, X, R, dY)
+    label = f"class_b={class_b} blocks={blocks} objects={objects}"
+    assert_close(from_em(dX), wantdX, label + " dX")
+    assert_close(from_em(dR), wantdR, label + " dR")
+    kb.close()
