@@ -293,15 +293,18 @@ __device__ __forceinline__ void store_row_buffer(__amdgpu_buffer_rsrc_t rsrc, ui
 // forward and dX passes: at most kMaxLdsB bytes per slice with 768-thread
 // workgroups, kMaxLdsBig with 1024; see launch_stream).
 //
-// The residual-hop variant with B in LDS (4 floats per lane, 8 or more lanes
-// per group) needs 84 VGPRs, four more than six waves per SIMD allow; it is
-// compiled for six waves (80 VGPRs, a few registers spilled), which measured
-// faster than keeping B in registers (large KB forward 0.89 -> 0.84 ms).  The
-// same cap on the soft-KB variants or on narrower lane groups spilled inside
-// the loop and ran slower, so they keep the compiler's own allocation.
+// The hard-KB variants with B in LDS (4 floats per lane; 8 lanes per group
+// with the paired entry fetch, 8 or more for the residual hop) need 83 or 84
+// VGPRs, more than six waves per SIMD allow; they are compiled for six waves
+// (80 VGPRs, a few registers spilled around the chunk loop, outside the
+// steps), which measured faster than losing the second workgroup per CU or
+// keeping B in registers (residual forward on the large KB 0.89 -> 0.84 ms).
+// The same cap on the soft-KB variants or on narrower lane groups spilled
+// inside the loop and ran slower, so they keep the compiler's own
+// allocation.
 template <int VEC, int LPT, bool WEIGHTED, bool RES, bool LDSB>
 constexpr int stream_min_waves() {
-  return (LDSB && RES && !WEIGHTED && VEC == 4 && LPT >= 8) ? 6 : 1;
+  return (LDSB && !WEIGHTED && VEC == 4 && (RES ? LPT >= 8 : LPT == 8)) ? 6 : 1;
 }
 
 template <int VEC, int LPT, bool BUF, bool WEIGHTED, bool RES, bool LDSB>
@@ -392,6 +395,19 @@ stream_kernel(StreamArgs a) {
       if constexpr (WEIGHTED) wmine[k] = a.weights[q];
     }
   };
+  // Two steps' entries, 2 per lane (entries p + 2l and p + 2l + 1 of lane
+  // l < kUnroll; lanes past it repeat the last pair).  p and the stream
+  // length are multiples of kUnroll, so every pair is 16-byte aligned and
+  // the clamp keeps it inside the stream.
+  // Only for groups of exactly eight lanes: not in the residual variants,
+  // whose register-capped LDS form spilled more with it and ran 0.7 % slower,
+  // nor with wider groups, whose LDS form would need the same cap and whose
+  // short chunks (small KBs) would then spill every other step.
+  constexpr bool kPairFetch = !WEIGHTED && !RES && K == 1 && LPT == kUnroll;
+  auto fetch2 = [&](int64_t p, int4 &mine) {
+    const int64_t q = min(p + 2 * min(lane, kUnroll - 1), a.n - 2);
+    mine = reinterpret_cast<const int4 *>(a.entries)[q / 2];
+  };
 
   for (int64_t g = c_begin + wg_in_list * GPB + grp; g < c_end; g += stride) {
     const int64_t p0 = KBF_CHECKED(g, a.n / a.chunk) * a.chunk;
@@ -405,20 +421,38 @@ stream_kernel(StreamArgs a) {
     }
 
     // Software pipeline: the entries of the next step are loaded while this
-    // step's gathers are in flight.
+    // step's gathers are in flight.  With lane groups of eight lanes or more
+    // (and no weights) one 16-byte load per lane fetches two steps' entries
+    // (lane l entries 2l and 2l + 1 of the pair), so the steps run in pairs
+    // and only the second of a pair issues a fetch: one entry load per two
+    // steps in front of their sixteen row gathers.
     int2 mine_next[K];
     float wmine_next[K];
-    fetch(p0, mine_next, wmine_next);
-    for (int64_t p = p0; p < p1; p += kUnroll) {
+    int4 mine2 = make_int4(0, 0, 0, 0);
+    if constexpr (kPairFetch)
+      fetch2(p0, mine2);
+    else
+      fetch(p0, mine_next, wmine_next);
+    // One step of kUnroll entries from p; H is its half of a pair (0 or 1)
+    // or -1 for the one-step fetch.
+    auto step = [&](const int64_t p, auto hc) {
+      constexpr int H = decltype(hc)::value;
       int2 e[kUnroll];
       float w[kUnroll];
       float xa[kUnroll][VEC], xb[kUnroll][VEC];
       static_for<kUnroll>([&](auto uc) {
         constexpr int u = decltype(uc)::value;
-        const int2 m = mine_next[u / LPT];
-        e[u] = make_int2(group_bcast<LPT, u % LPT>(m.x), group_bcast<LPT, u % LPT>(m.y));
-        if constexpr (WEIGHTED)
-          w[u] = __int_as_float(group_bcast<LPT, u % LPT>(__float_as_int(wmine_next[u / LPT])));
+        if constexpr (H >= 0) {
+          constexpr int src = (kUnroll / 2) * H + u / 2;
+          const int ex = (u % 2) ? mine2.z : mine2.x;
+          const int ey = (u % 2) ? mine2.w : mine2.y;
+          e[u] = make_int2(group_bcast<LPT, src>(ex), group_bcast<LPT, src>(ey));
+        } else {
+          const int2 m = mine_next[u / LPT];
+          e[u] = make_int2(group_bcast<LPT, u % LPT>(m.x), group_bcast<LPT, u % LPT>(m.y));
+          if constexpr (WEIGHTED)
+            w[u] = __int_as_float(group_bcast<LPT, u % LPT>(__float_as_int(wmine_next[u / LPT])));
+        }
       });
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
@@ -470,7 +504,10 @@ stream_kernel(StreamArgs a) {
                         xb[u]);
         }
       }
-      fetch(p + kUnroll, mine_next, wmine_next);
+      if constexpr (H < 0)
+        fetch(p + kUnroll, mine_next, wmine_next);
+      else if constexpr (H == 1)
+        fetch2(p + kUnroll, mine2);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const bool triple = e[u].x >= 0;
@@ -537,6 +574,16 @@ stream_kernel(StreamArgs a) {
         for (int v = 0; v < VEC; ++v) acc[v] = 0.0;
         }
       }
+    };
+    if constexpr (kPairFetch) {
+      // Chunks are whole steps; an odd last step runs alone.
+      for (int64_t p = p0; p < p1; p += 2 * kUnroll) {
+        step(p, std::integral_constant<int, 0>{});
+        if (p + kUnroll >= p1) break;
+        step(p + kUnroll, std::integral_constant<int, 1>{});
+      }
+    } else {
+      for (int64_t p = p0; p < p1; p += kUnroll) step(p, std::integral_constant<int, -1>{});
     }
   }
 }
