@@ -148,7 +148,9 @@ def test_argument_errors(kbf):
 @pytest.mark.parametrize("chunk,fan_in", [(2, 2), (8, 32), (16, 3), (24, 2), (40, 4), (64, 2), (4096, 32)])
 def test_chunk_and_combine_plans(kbf, chunk, fan_in, monkeypatch):
     # Tiny chunks put a marker every few entries: runs cut by chunk ends,
-    # no-op markers, rows split into many slots, deep combine trees.
+    # no-op markers, rows split into many slots, deep combine trees.  Chunks
+    # of an odd number of 8-entry steps end on a lone step of the paired
+    # entry fetch (8-lane groups: b = 7 and 32, and dR at b = 256).
     monkeypatch.setenv("KBFOLLOW_CHUNK", str(chunk))
     monkeypatch.setenv("KBFOLLOW_REL_CHUNK", str(chunk))
     monkeypatch.setenv("KBFOLLOW_FAN_IN", str(fan_in))
@@ -157,7 +159,7 @@ def test_chunk_and_combine_plans(kbf, chunk, fan_in, monkeypatch):
     s = np.concatenate([g.integers(0, n_e, 3000), np.full(700, 5)]).astype(np.int32)
     r = g.integers(0, n_r, len(s)).astype(np.int32)
     o = np.concatenate([g.integers(0, n_e, 3000), g.integers(0, 3, 700)]).astype(np.int32)
-    for b, exact in ((4, True), (12, False), (7, False)):
+    for b, exact in ((4, True), (12, False), (7, False), (32, True), (256, False)):
         if exact:
             X = (g.random((b, n_e)) < 0.2).astype(np.float32)
             R = np.zeros((b, n_r), np.float32)
