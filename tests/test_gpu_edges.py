@@ -185,3 +185,47 @@ def test_plain_load_path(kbf, b, monkeypatch):
     both(kbf, s, r, o, n_e, n_r, X, R, dY, False, f"plain loads b={b}")
     wt = np.random.default_rng(b).uniform(0.5, 1.5, len(s)).astype(np.float32)
     both(kbf, s, r, o, n_e, n_r, X, R, dY, False, f"plain loads weighted b={b}", weight=wt)
+
+
+@pytest.mark.parametrize("b", [1, 7, 32, 36, 256])
+def test_empty_rows_into_nan_outputs(kbf, b):
+    """Rows no triple reaches, in runs of one to three rows and one long run,
+    written into outputs prefilled with NaN (a row left unwritten stays NaN):
+    zeros from the plain passes, gamma * Z from the residual and
+    accumulating ones."""
+    import torch
+    n_e, n_r = 3000, 5
+    g = np.random.default_rng(700 + b)
+    ids = np.array([i for i in range(2000) if i % 7 in (0, 3, 4)], np.int32)
+    n_t = 12_000
+    s = g.choice(ids, n_t).astype(np.int32)
+    o = g.choice(ids, n_t).astype(np.int32)
+    r = g.integers(0, n_r, n_t).astype(np.int32)
+    s[:800] = ids[5]   # a hub row, split over chunks
+    o[800:1600] = ids[9]
+    X, R, dY = rand_io(b + 11, b, n_e, n_r)
+    Z = np.random.default_rng(b).standard_normal((b, n_e)).astype(np.float32)
+    kb = kbf.KB(s, r, o, n_e, n_r)
+    tX, tR, tdY, tZ = to_em(X), to_em(R), to_em(dY), to_em(Z)
+    nan = lambda t: torch.full_like(t, float("nan"))
+    Y = nan(tX)
+    kb.follow(tX, tR, out=Y)
+    Yr = nan(tX)
+    kb.follow(tX, tR, out=Yr, residual=0.5)
+    Ya = nan(tX)
+    kb.follow_accumulate(tX, tR, tZ, 0.25, out=Ya)
+    dX, dR = nan(tX), nan(tR)
+    kb.follow_backward(tX, tR, tdY, dX=dX, dR=dR)
+    torch.cuda.synchronize()
+    label = f"empty rows b={b}"
+    for name, t in (("Y", Y), ("residual", Yr), ("accumulate", Ya), ("dX", dX), ("dR", dR)):
+        assert not torch.isnan(t).any(), f"{label}: {name} has unwritten rows"
+    assert_close(from_em(Y), oracle.follow(s, r, o, n_e, n_r, X, R), label + " Y")
+    assert_close(from_em(Yr), oracle.follow_residual(s, r, o, n_e, n_r, X, R, gamma=0.5),
+                 label + " residual")
+    assert_close(from_em(Ya), oracle.follow_accumulate(s, r, o, n_e, n_r, X, R, Z, gamma=0.25),
+                 label + " accumulate")
+    wdX, wdR = oracle.follow_backward(s, r, o, n_e, n_r, X, R, dY)
+    assert_close(from_em(dX), wdX, label + " dX")
+    assert_close(from_em(dR), wdR, label + " dR")
+    kb.close()
